@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Benchmark: fused Λ24(12) dequantize + GEMV at batch 1 on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config c2_4096x4096]
+
+A step is one GEMV y = W x of the workload matrix in the served layout
+(Planes14, 4.80 b/w records + fp16 per-block scales), with W and x resident in
+HBM.  The timed region is exactly K steps, bracketed by a device
+synchronisation on both sides and timed with HIP events on the launch stream.
+Each step reads a different replica of the matrix (same codes, distinct
+buffers, ≥ 1 GB in total) so that the 256 MB Infinity Cache cannot serve
+repeated reads: the bytes come from HBM.
+
+Printed: one JSON line with the metric (served-weight GB/s of the Planes14
+GEMV), µs per GEMV, the roofline against MI355X's 8 TB/s, every arm of the
+layout comparison (four layouts, FP16 GEMV control, no-weights control;
+interleaved, 7 rounds, first 2 discarded, medians) and the CPU oracle timed on
+a bounded sample of the same workload.
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published peak
+REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Cache
+ARMS = ["planes14", "slot32", "planes12x", "golay70", "fp16", "noweights"]
+CONFIGS = {"c1_768x1536": (768, 1536), "c2_4096x4096": (4096, 4096),
+           "c4_8192x8192": (8192, 8192)}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[1])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--config", default="c2_4096x4096", choices=sorted(CONFIGS))
+    ap.add_argument("--arms", default=",".join(ARMS))
+    ap.add_argument("--rounds", type=int, default=7)
+    ap.add_argument("--discard", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--seed", type=int, default=0)
+    return ap.parse_args()
+
+
+class Arm:
+    """One arm: a list of replica launchers, each running one GEMV."""
+
+    def __init__(self, name, launchers, served_bytes, desc=None):
+        self.name, self.launchers, self.served_bytes, self.desc = name, launchers, served_bytes, desc
+
+    def run(self, k, start=0):
+        n = len(self.launchers)
+        for s in range(start, start + k):
+            self.launchers[s % n]()
+
+
+def build_arms(args, torch, P, synth):
+    M, K = CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    inp = synth.make_gemv_inputs(M, K, seed=args.seed, name=args.config)
+    cb = P.Codebook(12)
+    dcb = P.DeviceCodebook(cb, dev)
+    cls, sm, lv = cb.fields_from_points(inp.z)
+    log(f"[bench] inputs {M}x{K} (Kpad {inp.Kpad}) ready in {time.time() - t0:.1f}s")
+    x = torch.from_numpy(inp.x).to(dev)
+    y = torch.empty(M, dtype=torch.float32, device=dev)
+    arms = {}
+    wanted = args.arms.split(",")
+    base_desc = None
+    mat14 = None
+    for name in ("planes14", "slot32", "planes12x", "golay70"):
+        if name not in wanted and not (name == "planes14"):
+            continue
+        mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[name], cls, inp.gain, sm, lv, inp.scale, dev)
+        served = mat.desc.served_bytes
+        reps = max(1, math.ceil(REPLICA_BYTES / served))
+        mats = [mat] + [P.LeechMatrix(mat.desc, mat.main.clone(), mat.side0.clone(),
+                                      mat.side1.clone(), mat.scale.clone(), dcb)
+                        for _ in range(reps - 1)]
+        arms[name] = Arm(name, [(lambda m=m: m.gemv(x, y)) for m in mats], served, mat.desc)
+        if name == "planes14":
+            base_desc, mat14 = mat.desc, mat
+        log(f"[bench] {name}: {served} served bytes/GEMV, {reps} replicas")
+    if "fp16" in wanted:
+        # FP16 control on the same weights, decoded on the device
+        z, _, _ = mat14.decode()
+        zf = z.float()
+        fac = torch.from_numpy(inp.scale.astype("float32")).to(dev) / zf.pow(2).sum(-1).sqrt()
+        W = (zf * fac[..., None]).reshape(M, inp.Kpad).half().contiguous()
+        del z, zf
+        served = W.numel() * 2
+        reps = max(1, math.ceil(REPLICA_BYTES / served))
+        Ws = [W] + [W.clone() for _ in range(reps - 1)]
+        arms["fp16"] = Arm("fp16", [(lambda w=w: P.fp16_gemv(w, x, y)) for w in Ws], served)
+        log(f"[bench] fp16: {served} bytes/GEMV, {reps} replicas")
+    if "noweights" in wanted:
+        arms["noweights"] = Arm("noweights", [lambda: P.noweights_ctrl(base_desc, x, y)], 0)
+    return inp, arms
+
+
+def time_arm(torch, arm, steps, start=0):
+    st = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(st)
+    arm.run(steps, start)
+    e1.record(st)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1)          # ms for `steps` GEMVs
+
+
+def cpu_baseline(inp, seconds):
+    """The oracle as it stands, on the host: decode every block from its
+    fields, form the f64 weights and multiply, repeated for about `seconds`."""
+    import numpy as np
+    from oracle import decode as D
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    cls, sm, lv = D.fields_from_points(inp.z)           # setup, not timed
+    served = inp.M * inp.nb * 16
+    n, t0 = 0, time.perf_counter()
+    while True:
+        z = D.decode_fields(cls, sm, lv)
+        W = D.weights64(cls, inp.gain, inp.scale, z)
+        y = D.gemv64(W, inp.x)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or n >= 1000:
+            break
+    del y
+    return {"value": served * n / el / 1e9, "unit": "GB/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n} full {inp.M}x{inp.K} GEMVs on the host (oracle decode_fields + "
+                      f"weights64 + gemv64, f64), {el:.1f} s; GB/s of Planes14 served bytes",
+            "us_per_gemv": el / n * 1e6}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; the GEMV shards by "
+                          "rows or by K across GPUs (see the design notes) but no multi-GPU "
+                          "path is built", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import paper_2609_02652_amd as P
+    from paper_2609_02652_amd import synth
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU (torch.cuda.is_available() is False)")
+    inp, arms = build_arms(args, torch, P, synth)
+    main_arm = arms["planes14"]
+
+    # warmup every arm, then the contract's timed region: K Planes14 GEMVs
+    for a in arms.values():
+        a.run(args.warmup)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done; timing {args.steps} planes14 steps")
+    ms = time_arm(torch, main_arm, args.steps)
+    us = ms * 1e3 / args.steps
+    gbs = main_arm.served_bytes / (us * 1e-6) / 1e9
+
+    # layout comparison: arms interleaved in fixed order, rounds, first discarded
+    per_round = {n: [] for n in arms}
+    k_arm = max(50, args.steps // 4)
+    for r in range(args.rounds):
+        for n, a in arms.items():
+            per_round[n].append(time_arm(torch, a, k_arm) * 1e3 / k_arm)
+        log(f"[bench] round {r + 1}/{args.rounds} done")
+    kept = {n: v[args.discard:] for n, v in per_round.items()}
+    table = {}
+    for n, v in kept.items():
+        med = statistics.median(v)
+        row = {"us_per_gemv": round(med, 3), "min_us": round(min(v), 3), "max_us": round(max(v), 3),
+               "served_bytes": arms[n].served_bytes}
+        if arms[n].served_bytes:
+            row["GBps"] = round(arms[n].served_bytes / (med * 1e-6) / 1e9, 1)
+            row["pct_hbm_peak"] = round(100 * row["GBps"] / HBM_PEAK_GBS, 1)
+            row["bits_per_weight"] = round(8 * arms[n].served_bytes / (inp.M * inp.Kpad), 3)
+        if "fp16" in kept:
+            ratios = [f / t for f, t in zip(kept["fp16"], v)]
+            row["vs_fp16"] = round(statistics.median(ratios), 3)
+        table[n] = row
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f}s")
+        cpu = cpu_baseline(inp, args.cpu_seconds)
+
+    out = {
+        "metric": "Leech GEMV µs + served-weight GB/s (% HBM peak), batch 1, 4.80 bpw",
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms / args.steps, 6),
+        "us_per_gemv": round(us, 3),
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic: uniform Λ24(12) points, fp16 |N(0,1)|·0.02 block scales, fp16 N(0,1) x",
+        "config": {"workload": f"single GEMV W {inp.M}x{inp.K} (Kpad {inp.Kpad}), Planes14 + fp16 "
+                               f"block scales, batch 1", "M": inp.M, "K": inp.K, "Kpad": inp.Kpad,
+                   "layout": "planes14", "lane_cols": main_arm.desc.lane_cols,
+                   "served_bytes_per_gemv": main_arm.served_bytes,
+                   "replicas": len(main_arm.launchers)},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None},
+        "arms": table,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,215 @@
+/*
+ * leech.h — C ABI of libleech: fused multi-shell Λ24(12) dequantize + GEMV
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the batch-1 decode GEMV of "Unfolding the Leech
+ * Lattice: Fused Multi-Shell Decoding and VRAM Layouts for 2-Bit LLM Weights":
+ * weights are stored as 24-wide blocks, each the direction of a point of the
+ * ball Λ24(12) (301 classes, 111,043,117,458,000 points, §2.1) times a scale.
+ * An offline expansion turns each block's decoded fields (class id, gain bit,
+ * sign mask, magnitude level per coordinate, §2.2) into one of four VRAM
+ * layouts (§3.2); a HIP kernel reads a layout with shifts, masks and a table
+ * lookup that is the same on every lane, and computes y = W x (§2.3).
+ *
+ * Conventions used by every call
+ *   - Lattice points are integer vectors in the √8 scaling: shell m holds the
+ *     points with Σ z_i² = 16 m; the ball is shells 2..12.
+ *   - A class is a magnitude multiset.  Class ids follow the canonical order:
+ *     ascending (shell m, even before odd, magnitudes sorted descending and
+ *     compared lexicographically).  Ids 0..300; table slots 301..511 are zero.
+ *   - The level of a coordinate is the index of |z_i| among the class's
+ *     distinct magnitudes in ascending order (level 0 = smallest, 0 if the
+ *     class has zero coordinates).  Bit i of a sign mask is 1 iff z_i < 0 and
+ *     must be 0 where z_i = 0.
+ *   - Weight of block b, coordinate i:
+ *         w = scale_b · centroid[gain_b] · z_i / (4·√m_class)
+ *     with scale_b an IEEE binary16 value and centroid[] two f32 values.
+ *   - A matrix is M rows × Kpad columns, Kpad a multiple of 24, nb = Kpad/24
+ *     blocks per row; block (r, j) covers columns 24j .. 24j+23 of row r.
+ *     Host arrays of per-block fields are in row-major (r, j) order.
+ *   - x is binary16 of length Kpad (zero-padded past the logical K); y is f32.
+ *
+ * Return values: LEECH_OK (0) or a negative LEECH_E_* code; the message of the
+ * last failure on the calling thread is available from leech_last_error().
+ * No call aborts or exits the process.
+ *
+ * Memory: the caller owns every buffer it passes and every stream.  Host
+ * calls read and write host memory only.  Device calls take device pointers
+ * (hipMalloc'd or equivalent), enqueue work on the given stream (a hipStream_t
+ * passed as void*, NULL = the null stream) and return after enqueue; device
+ * calls allocate no device memory.
+ */
+#ifndef LEECH_H
+#define LEECH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+enum {
+  LEECH_OK = 0,
+  LEECH_E_ARG = -1,          /* null pointer or out-of-range scalar argument   */
+  LEECH_E_LAYOUT = -2,       /* unknown layout kind                             */
+  LEECH_E_SHAPE = -3,        /* M, Kpad or K not valid for the call             */
+  LEECH_E_FIELD = -4,        /* a block's decoded fields are not valid          */
+  LEECH_E_NOT_LATTICE = -5,  /* an integer vector is not a point of the ball    */
+  LEECH_E_HIP = -6,          /* a HIP runtime call or kernel launch failed      */
+  LEECH_E_CAPACITY = -7      /* an index field of the layout would overflow     */
+};
+
+/* Message describing the most recent failure on this thread ("" if none).
+ * The pointer stays valid until the next library call on this thread. */
+const char* leech_last_error(void);
+
+/* ----------------------------------------------------------- codebook
+ * The codebook of the ball Λ24(12) (§2.1, §2.3): the extended Golay code,
+ * the 301 classes with their sizes, and the tables the kernels read.
+ * Built on the host; immutable afterwards; safe to share between threads. */
+typedef struct leech_codebook leech_codebook;
+
+/* Build the codebook of the ball with shells 2..ball_m.  ball_m must be 12
+ * (the ball the paper serves, §2.1) or 13 (the class-cardinality lock N(13)
+ * of §2.4, for verification only; layouts and kernels need ball_m = 12). */
+int leech_codebook_build(int ball_m, leech_codebook** out);
+void leech_codebook_free(leech_codebook* cb);
+
+/* n_classes: 301 for ball_m = 12.  n_points: the number of lattice points of
+ * the ball, origin excluded (111043117458000).  index_bits: ceil(log2 N). */
+int leech_codebook_info(const leech_codebook* cb, int* n_classes, uint64_t* n_points,
+                        int* index_bits);
+
+/* Per-class facts for class_id < n_classes: shell m, parity (0 even / 1 odd),
+ * n_levels (1..5), levels[0..n_levels) = distinct magnitudes ascending,
+ * size = number of lattice points in the class. */
+int leech_codebook_class(const leech_codebook* cb, int class_id, int* shell, int* parity,
+                         int* n_levels, uint8_t levels[5], uint64_t* size);
+
+/* Tables held by the codebook, returned as a host pointer owned by the
+ * codebook (valid until leech_codebook_free) and its size in bytes.  Device
+ * calls take a device copy that the caller uploads.
+ *   LEECH_TABLE_CLASS_LEVELS: 512 records of 24 bytes — five f32 level values
+ *       a/(4√m) (round-to-nearest from f64) and a u32 level count, the class
+ *       table of §2.3; slots past the last class are zero.
+ *   LEECH_TABLE_CODEWORDS: 4096 u32, the extended Golay codewords sorted
+ *       ascending (bit i = coordinate i); the Golay70 layout's rank indexes it.
+ *   LEECH_TABLE_DEVICE: the table every GEMV/decode kernel reads: 512 records
+ *       of 32 bytes (see LEECH_DEVICE_TABLE_BYTES); pass its device copy as
+ *       d_class_table. */
+enum { LEECH_TABLE_CLASS_LEVELS = 0, LEECH_TABLE_CODEWORDS = 1, LEECH_TABLE_DEVICE = 2 };
+#define LEECH_TABLE_SLOTS 512
+#define LEECH_DEVICE_TABLE_BYTES (512 * 32)
+int leech_codebook_table(const leech_codebook* cb, int which, const void** host_ptr,
+                         size_t* nbytes);
+
+/* Decoded fields of n lattice points z (int8 [n][24], host).  Outputs (host,
+ * caller-allocated): class_id[n], sign_mask[n], level[n][24].  Fails with
+ * LEECH_E_NOT_LATTICE (first bad block index in the message) if a vector is
+ * not a point of the ball. */
+int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* z,
+                             uint16_t* class_id, uint32_t* sign_mask, uint8_t* level);
+
+/* ------------------------------------------------------------ layouts
+ * The four VRAM layouts of §3.2, all bit-exact (every block decodes to the
+ * same integer point, class and gain bit):
+ *   SLOT32     one-hot level masks (§3.2): class | gain | sign mask | one 24-bit
+ *              mask per level above level 0; 16-byte records (≤ 4 levels) or
+ *              20-byte records (5 levels); a side table locates each record.
+ *   PLANES14   three binary bit planes (§2.2, §2.3): a 112-bit record at a
+ *              uniform 14-byte stride; the served layout, 4.80 b/w.
+ *   PLANES12X  two bit planes in a 12-byte record for every block; blocks with
+ *              five levels also keep their exact PLANES14 record in an exception
+ *              table applied in the same launch (§3.2, sub-4.3 b/w).
+ *   GOLAY70    9-byte record: class | gain | 12-bit codeword rank | a 2-bit
+ *              in-class code per coordinate; blocks the 2-bit code cannot hold
+ *              are exceptions as in PLANES12X (§3.2, 3.6 b/w).
+ * Records are stored in "wave tile" order: rows are grouped in tiles of
+ * tile_rows = 64 / lane_cols rows; within a tile, each run of lane_cols
+ * consecutive blocks of the tile's rows forms one 64-block unit, stored row by
+ * row.  lane_cols (1, 2, 4, 8 or 16) is chosen from M so that a matrix has
+ * enough tiles to fill the GPU; the kernels read one unit per wavefront step.
+ */
+enum { LEECH_SLOT32 = 0, LEECH_PLANES14 = 1, LEECH_PLANES12X = 2, LEECH_GOLAY70 = 3 };
+
+typedef struct {
+  int32_t layout;          /* LEECH_* layout kind                               */
+  int32_t lane_cols;       /* blocks per row in one 64-block unit               */
+  int64_t M, Kpad, nb;     /* rows, padded columns, blocks per row              */
+  uint64_t main_bytes;     /* bytes of the main record stream (incl. 16-B pad)  */
+  uint64_t side_bytes[2];  /* side streams: exception table / per-tile offsets  */
+  uint64_t n_exceptions;   /* blocks served from the exception table           */
+  uint64_t served_bytes;   /* main + side streams + 2 B/block of fp16 scales   */
+} leech_layout_desc;
+
+/* Expand decoded fields into a layout (host, multithreaded).
+ * Inputs (host, row-major (r, j)): class_id[M·nb], gain_bit[M·nb] (0/1),
+ * sign_mask[M·nb], level[M·nb][24].  Every block is validated: class id in
+ * range, level < the class's level count, no sign bit on a zero coordinate,
+ * levels forming the class's magnitude multiset, no sign bits above bit 23;
+ * the first bad block is named in the error.
+ * Two-call protocol: with main_out == NULL only *desc is filled (sizes);
+ * otherwise main_out/side0_out/side1_out must hold desc->main_bytes /
+ * side_bytes[0] / side_bytes[1] bytes (a side pointer may be NULL when its
+ * size is 0).  Fails with LEECH_E_SHAPE if Kpad % 24 != 0 or M, Kpad ≤ 0,
+ * LEECH_E_LAYOUT for an unknown layout, LEECH_E_CAPACITY if a tile holds more
+ * exceptions than its index field can name. */
+int leech_expand_layout(const leech_codebook* cb, int layout, int64_t M, int64_t Kpad,
+                        const uint16_t* class_id, const uint8_t* gain_bit,
+                        const uint32_t* sign_mask, const uint8_t* level, void* main_out,
+                        void* side0_out, void* side1_out, leech_layout_desc* desc);
+
+/* Permute per-block fp16 scales (host, row-major (r, j)) into the layout's
+ * wave-tile order; scale_out holds M·nb binary16 values. */
+int leech_layout_scales(const leech_layout_desc* desc, const uint16_t* scale_rowmajor,
+                        uint16_t* scale_out);
+
+/* Host-side decode of a layout (for verification): integer coordinates
+ * z[M·nb][24], class_id[M·nb] and gain_bit[M·nb] in row-major (r, j) order.
+ * Any output pointer may be NULL. */
+int leech_host_decode_layout(const leech_codebook* cb, const leech_layout_desc* desc,
+                             const void* main, const void* side0, const void* side1,
+                             int8_t* z, uint16_t* class_id, uint8_t* gain_bit);
+
+/* --------------------------------------------------------- device calls */
+
+/* Fused dequantize + GEMV (§2.3): y[r] = Σ_j W[r][j] · x[j] with W decoded on
+ * the fly from the layout.  d_main/d_side0/d_side1: the layout's streams;
+ * d_class_table: device copy of LEECH_TABLE_DEVICE; d_codewords: device copy of
+ * LEECH_TABLE_CODEWORDS (GOLAY70 only, else may be NULL); d_scale: fp16 scales
+ * in wave-tile order (leech_layout_scales); centroid: the two f32 gain
+ * centroids; d_x: binary16 [Kpad]; d_y: f32 [M].  Accumulates in f32; the
+ * summation order depends only on (M, Kpad, lane_cols), so every layout of
+ * one matrix yields bit-identical y. */
+int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+               const void* d_side1, const void* d_class_table, const void* d_codewords,
+               const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
+               float* d_y, void* stream);
+
+/* Verification decode on the device with the GEMV's own decoders: z int8
+ * [M·nb][24], class_id [M·nb], gain_bit [M·nb], row-major (r, j).  Any output
+ * may be NULL. */
+int leech_decode_blocks(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                        const void* d_side1, const void* d_class_table,
+                        const void* d_codewords, int8_t* d_z, uint16_t* d_class_id,
+                        uint8_t* d_gain_bit, void* stream);
+
+/* FP16 GEMV control (§3.2, Table "layout scale" first row): y = W x with W a
+ * row-major binary16 [M][K] matrix, f32 accumulation.  K must be a multiple of
+ * 8 and d_W 16-byte aligned. */
+int leech_fp16_gemv_ref(int64_t M, int64_t K, const uint16_t* d_W, const uint16_t* d_x,
+                        float* d_y, void* stream);
+
+/* No-weights control (§3.3 "The no-weights control"): the GEMV's launch
+ * geometry, x staging and reductions for this layout's shape, reading no
+ * weight bytes: every block is taken as all-ones with unit scale, so
+ * y[r] = Σ_j x[j] (f32, the GEMV's summation order). */
+int leech_noweights_ctrl(const leech_layout_desc* desc, const uint16_t* d_x, float* d_y,
+                         void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LEECH_H */

@@ -236,3 +236,20 @@ def row_norms_from_scales(class_id, gain, scale_f16, centroids=(1.0, 1.0)) -> np
 
 def block_norm(z) -> float:
     return sqrt(float(sum(int(v) * int(v) for v in z)))
+
+
+def weights64_from_points(z, gain, scale_f16, centroids=(1.0, 1.0)) -> np.ndarray:
+    """Same weights as weights64, with each block's shell read off its point:
+    Σ z_i² = 16 m (§2.1), so the norm 4√m is √(Σ z_i²).  Lets the oracle follow
+    the full workload sizes without a per-block class lookup."""
+    z = np.asarray(z).astype(np.int64)
+    n2 = (z * z).sum(axis=-1)
+    if (n2 % 16).any() or (n2 < 32).any() or (n2 > 16 * BALL_M).any():
+        raise ValueError("a block is not a ball point")
+    g = np.asarray(gain).astype(np.int64)
+    s = np.asarray(scale_f16, dtype=np.float16).astype(np.float64)
+    cen = np.asarray(centroids, dtype=np.float32).astype(np.float64)
+    factor = s * cen[g] / np.sqrt(n2.astype(np.float64))
+    w = z.astype(np.float64) * factor[..., None]
+    M, nb = g.shape
+    return w.reshape(M, nb * DIM)

@@ -1,0 +1,125 @@
+"""MI355X-native fused Λ24(12) dequantize + GEMV (batch-1 decode).
+
+The compute path lives in libleech.so (include/leech.h): a C++ host half
+(codebook, decoded fields, offline layout expansion) and HIP kernels for
+gfx950 (fused GEMV per layout, verification decode, FP16 and no-weights
+controls).  This package is its thin binding; PyTorch only provides device
+memory and streams.  Importing it fails loudly if the library is not built.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import _lib
+from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, Codebook,
+                   LayoutDesc, LeechError, expand_layout, host_decode_layout, layout_scales)
+
+__all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
+           "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
+           "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl"]
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev(arr: np.ndarray, device):
+    torch = _torch()
+    t = torch.from_numpy(np.ascontiguousarray(arr).view(np.uint8))
+    return t.to(device)
+
+
+class DeviceCodebook:
+    """Device copies of the class table and the Golay codeword table."""
+
+    def __init__(self, cb: Codebook, device="cuda"):
+        self.cb = cb
+        self.table = _dev(cb.table(_lib.TABLE_DEVICE), device)
+        self.codewords = _dev(cb.table(_lib.TABLE_CODEWORDS), device)
+
+
+class LeechMatrix:
+    """One Leech-coded matrix resident in device memory in one layout."""
+
+    def __init__(self, desc: LayoutDesc, main, side0, side1, scale, dcb: DeviceCodebook):
+        self.desc, self.main, self.side0, self.side1, self.scale, self.dcb = (
+            desc, main, side0, side1, scale, dcb)
+
+    @classmethod
+    def from_fields(cls, dcb: DeviceCodebook, layout: int, class_id, gain, sign_mask, level,
+                    scale_rowmajor, device="cuda"):
+        desc, main, s0, s1 = expand_layout(dcb.cb, layout, class_id, gain, sign_mask, level)
+        sc = layout_scales(desc, scale_rowmajor)
+        torch = _torch()
+        empty = torch.empty(0, dtype=torch.uint8, device=device)
+        return cls(desc, _dev(main, device), _dev(s0, device) if s0.size else empty,
+                   _dev(s1, device) if s1.size else empty, _dev(sc, device), dcb)
+
+    @property
+    def M(self):
+        return self.desc.M
+
+    @property
+    def Kpad(self):
+        return self.desc.Kpad
+
+    def _ptrs(self):
+        return (self.main.data_ptr(), self.side0.data_ptr() if self.side0.numel() else 0,
+                self.side1.data_ptr() if self.side1.numel() else 0)
+
+    def gemv(self, x, y=None, centroids=(1.0, 1.0), stream=None):
+        """y = W x; x: fp16 [Kpad] device tensor, y: f32 [M] device tensor."""
+        torch = _torch()
+        if x.dtype != torch.float16 or x.numel() != self.Kpad or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 tensor of length Kpad")
+        if y is None:
+            y = torch.empty(self.M, dtype=torch.float32, device=x.device)
+        elif y.dtype != torch.float32 or y.numel() != self.M or not y.is_contiguous():
+            raise ValueError("y must be a contiguous f32 tensor of length M")
+        m, s0, s1 = self._ptrs()
+        _lib.gemv(self.desc, m, s0, s1, self.dcb.table.data_ptr(), self.dcb.codewords.data_ptr(),
+                  self.scale.data_ptr(), centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
+        return y
+
+    def decode(self, stream=None):
+        """Device decode: (z int8 [M, nb, 24], class_id int16 [M, nb], gain uint8 [M, nb])."""
+        torch = _torch()
+        M, nb = self.desc.M, self.desc.nb
+        dev = self.main.device
+        z = torch.empty((M, nb, 24), dtype=torch.int8, device=dev)
+        c = torch.empty((M, nb), dtype=torch.int16, device=dev)
+        g = torch.empty((M, nb), dtype=torch.uint8, device=dev)
+        m, s0, s1 = self._ptrs()
+        _lib.decode_blocks(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
+                           self.dcb.codewords.data_ptr(), z.data_ptr(), c.data_ptr(), g.data_ptr(),
+                           _stream(stream))
+        return z, c, g
+
+
+def fp16_gemv(W, x, y=None, stream=None):
+    """FP16 GEMV control: W fp16 [M, K] (K % 8 == 0), x fp16 [K] -> y f32 [M]."""
+    torch = _torch()
+    M, K = W.shape
+    if W.dtype != torch.float16 or x.dtype != torch.float16 or not W.is_contiguous():
+        raise ValueError("W and x must be contiguous fp16")
+    if y is None:
+        y = torch.empty(M, dtype=torch.float32, device=W.device)
+    _lib.fp16_gemv_ref(M, K, W.data_ptr(), x.data_ptr(), y.data_ptr(), _stream(stream))
+    return y
+
+
+def noweights_ctrl(desc: LayoutDesc, x, y=None, stream=None):
+    """No-weights control over the GEMV geometry of desc: y[r] = Σ x."""
+    torch = _torch()
+    if y is None:
+        y = torch.empty(desc.M, dtype=torch.float32, device=x.device)
+    _lib.noweights_ctrl(desc, x.data_ptr(), y.data_ptr(), _stream(stream))
+    return y

@@ -1,0 +1,206 @@
+"""ctypes binding of libleech (include/leech.h): argument marshalling only.
+
+Every step of the GEMV path runs in the library: host calls in its C++ half,
+device calls in its HIP kernels.  PyTorch supplies device memory and streams.
+If libleech.so is missing this module raises at import: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libleech.so")
+
+SLOT32, PLANES14, PLANES12X, GOLAY70 = 0, 1, 2, 3
+LAYOUTS = {"slot32": SLOT32, "planes14": PLANES14, "planes12x": PLANES12X, "golay70": GOLAY70}
+LAYOUT_NAMES = {v: k for k, v in LAYOUTS.items()}
+TABLE_CLASS_LEVELS, TABLE_CODEWORDS, TABLE_DEVICE = 0, 1, 2
+ERRORS = {0: "OK", -1: "LEECH_E_ARG", -2: "LEECH_E_LAYOUT", -3: "LEECH_E_SHAPE",
+          -4: "LEECH_E_FIELD", -5: "LEECH_E_NOT_LATTICE", -6: "LEECH_E_HIP",
+          -7: "LEECH_E_CAPACITY"}
+EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
+           "leech_codebook_info", "leech_codebook_class", "leech_codebook_table",
+           "leech_fields_from_points", "leech_expand_layout", "leech_layout_scales",
+           "leech_host_decode_layout", "leech_gemv", "leech_decode_blocks",
+           "leech_fp16_gemv_ref", "leech_noweights_ctrl"]
+
+
+class LeechError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class LayoutDesc(C.Structure):
+    _fields_ = [("layout", C.c_int32), ("lane_cols", C.c_int32), ("M", C.c_int64),
+                ("Kpad", C.c_int64), ("nb", C.c_int64), ("main_bytes", C.c_uint64),
+                ("side_bytes", C.c_uint64 * 2), ("n_exceptions", C.c_uint64),
+                ("served_bytes", C.c_uint64)]
+
+    def as_dict(self) -> dict:
+        return {"layout": LAYOUT_NAMES.get(self.layout, self.layout), "lane_cols": self.lane_cols,
+                "M": self.M, "Kpad": self.Kpad, "nb": self.nb, "main_bytes": self.main_bytes,
+                "side_bytes": [self.side_bytes[0], self.side_bytes[1]],
+                "n_exceptions": self.n_exceptions, "served_bytes": self.served_bytes}
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2609_02652_amd.build` (no CPU fallback exists)")
+    lib = C.CDLL(LIB_PATH)
+    P, I64, U64, I = C.c_void_p, C.c_int64, C.c_uint64, C.c_int
+    sig = {
+        "leech_last_error": (C.c_char_p, []),
+        "leech_codebook_build": (I, [I, C.POINTER(P)]),
+        "leech_codebook_free": (None, [P]),
+        "leech_codebook_info": (I, [P, C.POINTER(I), C.POINTER(U64), C.POINTER(I)]),
+        "leech_codebook_class": (I, [P, I, C.POINTER(I), C.POINTER(I), C.POINTER(I), P,
+                                     C.POINTER(U64)]),
+        "leech_codebook_table": (I, [P, I, C.POINTER(P), C.POINTER(C.c_size_t)]),
+        "leech_fields_from_points": (I, [P, I64, P, P, P, P]),
+        "leech_expand_layout": (I, [P, I, I64, I64, P, P, P, P, P, P, P, C.POINTER(LayoutDesc)]),
+        "leech_layout_scales": (I, [C.POINTER(LayoutDesc), P, P]),
+        "leech_host_decode_layout": (I, [P, C.POINTER(LayoutDesc), P, P, P, P, P, P]),
+        "leech_gemv": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P, P]),
+        "leech_decode_blocks": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P]),
+        "leech_fp16_gemv_ref": (I, [I64, I64, P, P, P, P]),
+        "leech_noweights_ctrl": (I, [C.POINTER(LayoutDesc), P, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+
+
+def check(rc: int) -> None:
+    if rc != 0:
+        raise LeechError(rc, lib.leech_last_error().decode(errors="replace"))
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    if not a.flags["C_CONTIGUOUS"]:
+        raise ValueError("array must be C-contiguous")
+    return a.ctypes.data_as(C.c_void_p)
+
+
+# ------------------------------------------------------------------ codebook
+class Codebook:
+    """Host codebook of the ball (leech_codebook_*)."""
+
+    def __init__(self, ball_m: int = 12):
+        h = C.c_void_p()
+        check(lib.leech_codebook_build(ball_m, C.byref(h)))
+        self._h = h
+        self.ball_m = ball_m
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            lib.leech_codebook_free(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    def info(self) -> dict:
+        n, pts, bits = C.c_int(), C.c_uint64(), C.c_int()
+        check(lib.leech_codebook_info(self._h, C.byref(n), C.byref(pts), C.byref(bits)))
+        return {"n_classes": n.value, "n_points": pts.value, "index_bits": bits.value}
+
+    def class_info(self, cid: int) -> dict:
+        sh, par, nl, sz = C.c_int(), C.c_int(), C.c_int(), C.c_uint64()
+        lv = (C.c_uint8 * 5)()
+        check(lib.leech_codebook_class(self._h, cid, C.byref(sh), C.byref(par), C.byref(nl),
+                                       C.cast(lv, C.c_void_p), C.byref(sz)))
+        return {"shell": sh.value, "parity": par.value, "n_levels": nl.value,
+                "levels": tuple(lv[: nl.value]), "size": sz.value}
+
+    def table(self, which: int) -> np.ndarray:
+        p, n = C.c_void_p(), C.c_size_t()
+        check(lib.leech_codebook_table(self._h, which, C.byref(p), C.byref(n)))
+        return np.ctypeslib.as_array(C.cast(p, C.POINTER(C.c_uint8)), shape=(n.value,)).copy()
+
+    def fields_from_points(self, z: np.ndarray):
+        z = np.ascontiguousarray(z, dtype=np.int8)
+        shp = z.shape[:-1]
+        n = int(np.prod(shp)) if shp else 1
+        cls = np.empty(n, np.uint16)
+        sm = np.empty(n, np.uint32)
+        lv = np.empty((n, 24), np.uint8)
+        check(lib.leech_fields_from_points(self._h, n, _ptr(z), _ptr(cls), _ptr(sm), _ptr(lv)))
+        return cls.reshape(shp), sm.reshape(shp), lv.reshape(shp + (24,))
+
+
+# ------------------------------------------------------------------- layouts
+def expand_layout(cb: Codebook, layout: int, class_id, gain, sign_mask, level):
+    """Fields (row-major [M, nb]) -> (desc, main, side0, side1) host byte arrays."""
+    class_id = np.ascontiguousarray(class_id, np.uint16)
+    gain = np.ascontiguousarray(gain, np.uint8)
+    sign_mask = np.ascontiguousarray(sign_mask, np.uint32)
+    level = np.ascontiguousarray(level, np.uint8)
+    M, nb = class_id.shape
+    d = LayoutDesc()
+    args = (cb.handle, layout, M, nb * 24, _ptr(class_id), _ptr(gain), _ptr(sign_mask), _ptr(level))
+    check(lib.leech_expand_layout(*args, None, None, None, C.byref(d)))
+    main = np.zeros(d.main_bytes, np.uint8)
+    s0 = np.zeros(max(d.side_bytes[0], 1), np.uint8)
+    s1 = np.zeros(max(d.side_bytes[1], 1), np.uint8)
+    check(lib.leech_expand_layout(*args, _ptr(main), _ptr(s0), _ptr(s1), C.byref(d)))
+    return d, main, s0[: d.side_bytes[0]], s1[: d.side_bytes[1]]
+
+
+def layout_scales(desc: LayoutDesc, scale_rowmajor: np.ndarray) -> np.ndarray:
+    s = np.ascontiguousarray(scale_rowmajor, np.float16).view(np.uint16)
+    out = np.empty(desc.M * desc.nb, np.uint16)
+    check(lib.leech_layout_scales(C.byref(desc), _ptr(s), _ptr(out)))
+    return out.view(np.float16)
+
+
+def host_decode_layout(cb: Codebook, desc: LayoutDesc, main, side0, side1):
+    n = desc.M * desc.nb
+    z = np.empty((n, 24), np.int8)
+    cls = np.empty(n, np.uint16)
+    g = np.empty(n, np.uint8)
+    s0 = _ptr(side0) if side0 is not None and side0.size else None
+    s1 = _ptr(side1) if side1 is not None and side1.size else None
+    check(lib.leech_host_decode_layout(cb.handle, C.byref(desc), _ptr(main), s0, s1,
+                                       _ptr(z), _ptr(cls), _ptr(g)))
+    shp = (desc.M, desc.nb)
+    return z.reshape(shp + (24,)), cls.reshape(shp), g.reshape(shp)
+
+
+# -------------------------------------------------------------- device calls
+# Device pointers are integers (torch tensor .data_ptr()); stream is a raw
+# hipStream_t integer (torch.cuda.Stream.cuda_stream) or 0.
+def gemv(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroids, d_x, d_y,
+         stream=0):
+    cen = (C.c_float * 2)(float(centroids[0]), float(centroids[1]))
+    check(lib.leech_gemv(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
+                         d_codewords or None, d_scale, C.cast(cen, C.c_void_p), d_x, d_y,
+                         stream or None))
+
+
+def decode_blocks(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_z, d_cls, d_gain,
+                  stream=0):
+    check(lib.leech_decode_blocks(C.byref(desc), d_main, d_side0 or None, d_side1 or None,
+                                  d_table, d_codewords or None, d_z or None, d_cls or None,
+                                  d_gain or None, stream or None))
+
+
+def fp16_gemv_ref(M, K, d_W, d_x, d_y, stream=0):
+    check(lib.leech_fp16_gemv_ref(M, K, d_W, d_x, d_y, stream or None))
+
+
+def noweights_ctrl(desc, d_x, d_y, stream=0):
+    check(lib.leech_noweights_ctrl(C.byref(desc), d_x, d_y, stream or None))

@@ -1,0 +1,83 @@
+// Internal declarations shared by the host (host.cpp) and device (kernels.hip)
+// halves of libleech.  Not part of the public ABI (include/leech.h).
+#pragma once
+
+#include <algorithm>
+#include <cstdint>
+#include <string>
+
+#include "leech.h"
+
+namespace leech {
+
+constexpr int kDim = 24;
+constexpr int kMaxLevels = 5;
+constexpr int kTableSlots = LEECH_TABLE_SLOTS;
+constexpr int kWave = 64;
+constexpr int kPadBytes = 16;        // trailing zero bytes after every record stream
+
+// Record widths of the four layouts (bytes).
+constexpr int kPlanes14Bytes = 14;
+constexpr int kPlanes12Bytes = 12;
+constexpr int kGolay70Bytes = 9;
+constexpr int kSlot32Small = 16;     // ≤ 4 levels
+constexpr int kSlot32Large = 20;     // 5 levels
+constexpr int kUnitEntryBytes = 16;  // per-unit side entry: u64 bitmap, u32 base, u32 zero
+
+// Planes12x: the spare bits [82, 96) of the 12-byte record hold 1 + the
+// block's index in its tile's exception list, or 0.
+constexpr int kP12ExcShift = 82 - 64;          // bit position inside word 2
+constexpr uint32_t kP12ExcMax = (1u << 14) - 2; // largest storable local index
+
+// Device class record: 32 bytes per class id (LEECH_DEVICE_TABLE_BYTES / 512).
+//   mag[8]      : |z| of each level code 0..7 (codes ≥ n_levels are 0)
+//   inv_norm    : f32 of 1 / (4 √m)
+//   info        : n_levels | parity << 8 | shell << 16
+//   g70[2][4]   : Golay70 signed values, [side][2-bit code]
+//   reserved[8] : zero
+struct DevClass {
+  uint8_t mag[8];
+  float inv_norm;
+  uint32_t info;
+  int8_t g70[2][4];
+  uint8_t reserved[8];
+};
+static_assert(sizeof(DevClass) == 32, "device class record is 32 bytes");
+
+// Geometry shared by the expansion and the kernels: rows are grouped into
+// tiles of tile_rows = 64 / lane_cols rows; a unit is the 64 (or fewer, at the
+// edges) blocks of one tile × lane_cols consecutive block columns, stored row
+// by row.  Units of a tile are stored in column order; tiles in row order.
+struct Geometry {
+  int64_t M, nb;
+  int C;            // lane_cols
+  int R;            // tile_rows = 64 / C
+  int64_t tiles;    // ceil(M / R)
+  int64_t groups;   // units per tile = ceil(nb / C)
+
+  Geometry(int64_t M_, int64_t nb_, int C_)
+      : M(M_), nb(nb_), C(C_), R(kWave / C_), tiles((M_ + kWave / C_ - 1) / (kWave / C_)),
+        groups((nb_ + C_ - 1) / C_) {}
+  int rows_in_tile(int64_t t) const { return (int)std::min<int64_t>(R, M - t * R); }
+  int cols_in_group(int64_t g) const { return (int)std::min<int64_t>(C, nb - g * C); }
+  // first block index of unit (t, g) in storage order
+  int64_t unit_base(int64_t t, int64_t g) const {
+    return t * (int64_t)R * nb + g * (int64_t)rows_in_tile(t) * C;
+  }
+  // storage index of block (r, j)
+  int64_t index(int64_t r, int64_t j) const {
+    int64_t t = r / R, g = j / C;
+    return unit_base(t, g) + (r % R) * cols_in_group(g) + (j % C);
+  }
+  // sequential unit number (t * groups + g): Slot32/Golay70 side entries
+  int64_t unit_id(int64_t t, int64_t g) const { return t * groups + g; }
+  int64_t units() const { return tiles * groups; }
+};
+
+int choose_lane_cols(int64_t M);
+
+// thread-local error reporting
+int set_error(int code, const std::string& msg);
+void clear_error();
+
+}  // namespace leech

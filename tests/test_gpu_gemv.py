@@ -1,0 +1,173 @@
+"""GPU parity: the HIP path through the C ABI against the oracle.
+
+* decoded blocks (integer coordinates, class id, gain bit) are bit-exact
+  against the drawn points and the oracle's fields, for every layout;
+* y is within max|y − y64| / (‖W_r‖·‖x‖) ≤ 2e-3 of the oracle's f64 matvec
+  (and, reported beside it, within the paper's 1e-5·Σ|w·x| per row, §2.4);
+* every layout of one matrix yields bit-identical y;
+* the FP16 control and the no-weights control against their own f64 sums.
+Sizes span several tiles with ragged row tiles and ragged block columns, the
+workload shapes 768×1536 and 4096×4096, and the full 8192×8192 layout sweep.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import paper_2609_02652_amd as P  # noqa: E402
+from paper_2609_02652_amd import synth  # noqa: E402
+from oracle import decode as D  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+TOL_NORM = 2e-3      # max|y − y64| / (‖W_r‖₂ ‖x‖₂)
+TOL_PAPER = 1e-5     # |y − y64| / Σ_j |W_rj x_j|  (§2.4)
+CEN = (0.75, 1.25)   # distinct gain centroids so the gain bit matters
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def dcb(dev):
+    return P.DeviceCodebook(P.Codebook(12), dev)
+
+
+_cache = {}
+
+
+def case(M, K, seed):
+    key = (M, K, seed)
+    if key not in _cache:
+        inp = synth.make_gemv_inputs(M, K, seed=seed, name=f"gpu{M}x{K}")
+        cb = P.Codebook(12)
+        fields = cb.fields_from_points(inp.z)
+        _cache[key] = (inp, fields)
+    return _cache[key]
+
+
+SMALL = [(1, 24), (3, 48), (65, 24 * 17), (100, 500), (257, 24 * 33), (768, 1536)]
+
+
+@pytest.mark.parametrize("layout", list(P.LAYOUTS))
+@pytest.mark.parametrize("M,K", SMALL + [(4096, 4096)])
+def test_decode_bit_exact(dev, dcb, layout, M, K):
+    inp, (cls, sm, lv) = case(M, K, 1)
+    say(f"[decode] layout={layout} M={M} K={K}")
+    if M * inp.nb <= 20000:
+        oc, osm, olv = D.fields_from_points(inp.z)          # oracle's fields
+        assert (oc == cls).all() and (osm == sm).all() and (olv == lv).all()
+    mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[layout], cls, inp.gain, sm, lv, inp.scale, dev)
+    z, c, g = mat.decode()
+    torch.cuda.synchronize()
+    assert (z.cpu().numpy() == inp.z).all()
+    assert (c.cpu().numpy().astype(np.uint16) == cls).all()
+    assert (g.cpu().numpy() == inp.gain).all()
+
+
+def oracle_y(inp, centroids):
+    W = D.weights64_from_points(inp.z, inp.gain, inp.scale, centroids)
+    return W, D.gemv64(W, inp.x)
+
+
+@pytest.mark.parametrize("layout", list(P.LAYOUTS))
+@pytest.mark.parametrize("M,K", SMALL + [(4096, 4096)])
+def test_gemv_matches_oracle(dev, dcb, layout, M, K):
+    inp, (cls, sm, lv) = case(M, K, 1)
+    say(f"[gemv] layout={layout} M={M} K={K}")
+    mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[layout], cls, inp.gain, sm, lv, inp.scale, dev)
+    x = torch.from_numpy(inp.x).to(dev)
+    y = mat.gemv(x, centroids=CEN)
+    torch.cuda.synchronize()
+    W, y64 = oracle_y(inp, CEN)
+    e = D.errors(y.cpu().numpy(), y64, W, inp.x)
+    say(f"    errors {e}")
+    assert e["max_norm_err"] <= TOL_NORM
+    assert e["max_abs_err"] <= TOL_PAPER
+
+
+@pytest.mark.parametrize("M,K", [(257, 24 * 33), (768, 1536), (8192, 8192)])
+def test_layouts_bit_identical(dev, dcb, M, K):
+    """Layout sweep: the same codes served four ways give bit-identical y."""
+    inp, (cls, sm, lv) = case(M, K, 2)
+    x = torch.from_numpy(inp.x).to(dev)
+    ys = {}
+    for name, lay in P.LAYOUTS.items():
+        say(f"[sweep] layout={name} M={M} K={K}")
+        mat = P.LeechMatrix.from_fields(dcb, lay, cls, inp.gain, sm, lv, inp.scale, dev)
+        ys[name] = mat.gemv(x, centroids=(1.0, 1.0)).cpu().numpy()
+        if M * inp.nb > 1_000_000:                          # full-size decode check
+            z, c, g = mat.decode()
+            assert torch.equal(z.cpu(), torch.from_numpy(inp.z))
+        del mat
+        torch.cuda.empty_cache()
+    ref = ys["planes14"].view(np.uint32)
+    for name, y in ys.items():
+        assert (y.view(np.uint32) == ref).all(), name
+    # and against the oracle on a sample of rows (every row when small)
+    rows = np.arange(M) if M <= 1024 else np.random.default_rng(0).choice(M, 256, replace=False)
+    sub = synth.GemvInputs(len(rows), inp.K, inp.Kpad, inp.nb, inp.z[rows], inp.gain[rows],
+                           inp.scale[rows], inp.x, inp.seed, inp.name)
+    W, y64 = oracle_y(sub, (1.0, 1.0))
+    e = D.errors(ys["planes14"][rows], y64, W, inp.x)
+    say(f"    errors {e}")
+    assert e["max_norm_err"] <= TOL_NORM and e["max_abs_err"] <= TOL_PAPER
+
+
+def test_one_hot_columns(dev, dcb):
+    """x = e_j extracts column j: one exact dot product times the block factor."""
+    inp, (cls, sm, lv) = case(100, 500, 1)
+    mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    W, _ = oracle_y(inp, CEN)
+    for j in (0, 1, 23, 24, 250, 499):
+        say(f"[onehot] column {j}")
+        e = np.zeros(inp.Kpad, np.float16)
+        e[j] = 1
+        y = mat.gemv(torch.from_numpy(e).to(dev), centroids=CEN).cpu().numpy().astype(np.float64)
+        # f32 rounding of scale·centroid and of the product with 1/(4√m): ≤ 3 ulp
+        assert np.all(np.abs(y - W[:, j]) <= 3 * np.spacing(np.abs(W[:, j]).astype(np.float32)))
+
+
+def test_repeat_is_deterministic(dev, dcb):
+    inp, (cls, sm, lv) = case(768, 1536, 1)
+    mat = P.LeechMatrix.from_fields(dcb, P.GOLAY70, cls, inp.gain, sm, lv, inp.scale, dev)
+    x = torch.from_numpy(inp.x).to(dev)
+    a = mat.gemv(x).cpu().numpy()
+    b = mat.gemv(x).cpu().numpy()
+    assert (a.view(np.uint32) == b.view(np.uint32)).all()
+
+
+@pytest.mark.parametrize("M,K", [(1, 8), (7, 24), (768, 1536), (4096, 4104)])
+def test_fp16_control(dev, M, K):
+    say(f"[fp16] M={M} K={K}")
+    rng = np.random.default_rng(M + K)
+    W = (rng.standard_normal((M, K)) * 0.05).astype(np.float16)
+    x = rng.standard_normal(K).astype(np.float16)
+    y = P.fp16_gemv(torch.from_numpy(W).to(dev), torch.from_numpy(x).to(dev)).cpu().numpy()
+    W64 = W.astype(np.float64)
+    y64 = W64 @ x.astype(np.float64)
+    e = D.errors(y, y64, W64, x)
+    assert e["max_abs_err"] <= TOL_PAPER
+
+
+@pytest.mark.parametrize("M,K", [(65, 24 * 17), (4096, 4096)])
+def test_noweights_control(dev, dcb, M, K):
+    say(f"[noweights] M={M} K={K}")
+    inp, (cls, sm, lv) = case(M, K, 1)
+    d = P.expand_layout(dcb.cb, P.PLANES14, cls, inp.gain, sm, lv)[0]
+    y = P.noweights_ctrl(d, torch.from_numpy(inp.x).to(dev)).cpu().numpy().astype(np.float64)
+    want = inp.x.astype(np.float64).sum()
+    scale = np.abs(inp.x.astype(np.float64)).sum()
+    assert np.all(np.abs(y - want) <= 1e-5 * scale)
+    assert np.all(y == y[0])              # the same sum in every row

@@ -178,3 +178,11 @@ def test_planted_normalisation_is_caught(pts):
     assert not np.allclose(np.sqrt((wrong ** 2).sum(1)), 1.0)
     right = z / (4 * np.sqrt(shell))[:, None]
     assert np.allclose(np.sqrt((right ** 2).sum(1)), 1.0, rtol=1e-15)
+
+
+def test_weights_from_points_equal_class_weights():
+    inp = synth.make_gemv_inputs(6, 240, seed=13, name="wfp")
+    cid, sm, lv = D.fields_from_points(inp.z)
+    W1 = D.weights64(cid, inp.gain, inp.scale, inp.z, centroids=(0.5, 2.0))
+    W2 = D.weights64_from_points(inp.z, inp.gain, inp.scale, centroids=(0.5, 2.0))
+    assert np.allclose(W1, W2, rtol=1e-15, atol=0)
