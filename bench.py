@@ -55,15 +55,26 @@ def parse():
 
 
 class Arm:
-    """One arm: a list of replica launchers, each running one GEMV."""
+    """One arm: a list of replica launchers, each enqueueing one GEMV."""
 
     def __init__(self, name, launchers, served_bytes, desc=None):
         self.name, self.launchers, self.served_bytes, self.desc = name, launchers, served_bytes, desc
+        self._graphs = {}
 
     def run(self, k, start=0):
         n = len(self.launchers)
         for s in range(start, start + k):
             self.launchers[s % n]()
+
+    def graph(self, torch, k):
+        """A HIP graph of k consecutive GEMVs (replicas in turn), captured once:
+        replaying it enqueues the k kernels without k host round trips."""
+        if k not in self._graphs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self.run(k)
+            self._graphs[k] = g
+        return self._graphs[k]
 
 
 def build_arms(args, torch, P, synth):
@@ -111,16 +122,20 @@ def build_arms(args, torch, P, synth):
     return inp, arms
 
 
-def time_arm(torch, arm, steps, start=0):
+def time_arm(torch, arm, steps):
+    """ms for `steps` GEMVs: one replay of a graph holding exactly `steps`
+    launches, bracketed by device synchronisations and timed with HIP events
+    on the stream the kernels run on."""
+    g = arm.graph(torch, steps)
     st = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(st)
-    arm.run(steps, start)
+    g.replay()
     e1.record(st)
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1)          # ms for `steps` GEMVs
+    return e0.elapsed_time(e1)
 
 
 def cpu_baseline(inp, seconds):
@@ -167,9 +182,13 @@ def main():
     inp, arms = build_arms(args, torch, P, synth)
     main_arm = arms["planes14"]
 
-    # warmup every arm, then the contract's timed region: K Planes14 GEMVs
+    # warmup every arm (eager, then its graphs), then the contract's timed
+    # region: K Planes14 GEMVs
+    k_arm = max(50, args.steps // 4)
     for a in arms.values():
         a.run(args.warmup)
+        a.graph(torch, k_arm).replay()
+    main_arm.graph(torch, args.steps).replay()
     torch.cuda.synchronize()
     log(f"[bench] warmup done; timing {args.steps} planes14 steps")
     ms = time_arm(torch, main_arm, args.steps)
@@ -178,7 +197,6 @@ def main():
 
     # layout comparison: arms interleaved in fixed order, rounds, first discarded
     per_round = {n: [] for n in arms}
-    k_arm = max(50, args.steps // 4)
     for r in range(args.rounds):
         for n, a in arms.items():
             per_round[n].append(time_arm(torch, a, k_arm) * 1e3 / k_arm)

@@ -9,23 +9,29 @@
 // used).  A workgroup owns one tile of tile_rows = 64 / lane_cols rows and
 // walks its units: a unit is the ≤ 64 blocks of the tile's rows in lane_cols
 // consecutive block columns, stored contiguously, so one wavefront step loads
-// one unit with fully coalesced 128-byte lines (896 bytes of Planes14 records
-// and 128 bytes of fp16 scales per step).  Lane (r, c) of a step handles block
-// (tile·R + r, g·C + c) and accumulates its row's partial sum in a register;
-// the activation x (binary16) and the class table are staged in LDS once per
-// workgroup.  At the end the C lanes of a row are summed by an xor butterfly
-// and the waves of the workgroup through LDS, in a fixed order, so the result
-// depends only on (M, Kpad, lane_cols) and not on the layout.
+// one unit with coalesced 128-byte lines (896 bytes of Planes14 records and
+// 128 bytes of fp16 scales).  Each wavefront keeps kPrefetch units in flight:
+// their loads are issued before the workgroup stages x and the class table in
+// LDS, and every step refills the slot it consumed.  Lane (r, c) of a step
+// handles block (tile·R + r, g·C + c) and keeps its row's partial sum in a
+// register; at the end the C lanes of a row are summed by an xor butterfly and
+// the waves through LDS, in a fixed order, so y depends only on
+// (M, Kpad, lane_cols), never on the layout.
 //
-// Every block is decoded to 12 packed binary16 pairs of its signed integer
-// coordinates z_i (|z_i| ≤ 13, exact in binary16) and multiplied with x by
-// v_dot2_f32_f16 (exact products, f32 sums); the block's factor
-// scale · centroid[gain] / (4√m) is applied once per block (§2.3: one
-// multiply per block).
+// Decode.  The paper's per-coordinate predicated tree is replaced, since the
+// MI355X has about an order of magnitude less VALU issue per HBM byte than the
+// paper's GPU: the four 24-bit planes of a block (p0, p1, p2 and the inverted
+// sign mask) are transposed 4×4 inside every nibble with eight v_bfi_b32,
+// giving one nibble per coordinate; a v_perm_b32 byte lookup in the class's
+// 8-byte table then yields two binary16 values at once, each the coordinate's
+// magnitude |z| as a subnormal (|z|·2^-24, exact) with the sign in bit 15.
+// v_dot2_f32_f16 multiplies them with x exactly and sums in f32; the block's
+// factor 2^24 · scale · centroid[gain] / (4√m) is applied once per block.
 
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 
@@ -39,6 +45,8 @@ typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
 typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));
 
 constexpr int kNoWeights = 99;   // layout id of the no-weights control
+constexpr int kPrefetch = 8;     // units in flight per wavefront
+constexpr float kTwo24 = 16777216.0f;
 
 struct GemvArgs {
   const uint8_t* main;
@@ -54,266 +62,508 @@ struct GemvArgs {
   int C, R, waves;
 };
 
+// Per-(class, gain) entry staged in LDS; e = class | gain << 9.
+struct LdsEntry {
+  uint32_t tlo, thi;    // v_perm table (DevClass::perm)
+  float factor;         // 2^24 · centroid[gain] / (4√m)
+  uint32_t nlev;        // level count
+};
+// Golay70 per-class entry staged in LDS (index = class id).
+struct G70Entry {
+  uint32_t alo, ahi;    // |value| at side·4 + code
+  uint32_t slo, shi;    // 0x80 where that value is negative
+};
+
 __device__ __forceinline__ uint32_t align(uint32_t hi, uint32_t lo, uint32_t s) {
   return __builtin_amdgcn_alignbit(hi, lo, s);
 }
-
-__device__ __forceinline__ half2_t pack2(int a, int b) {
-  return __builtin_bit_cast(half2_t, __builtin_amdgcn_cvt_pkrtz((float)a, (float)b));
+__device__ __forceinline__ uint32_t perm(uint32_t s0, uint32_t s1, uint32_t sel) {
+  return __builtin_amdgcn_perm(s0, s1, sel);
 }
-
+__device__ __forceinline__ uint32_t bfi(uint32_t m, uint32_t a, uint32_t b) {
+  return (m & a) | (~m & b);
+}
 // Reinterpret a 32-bit word as two binary16 values.  Takes the word by value:
 // applying __builtin_bit_cast directly to an ext_vector element (w.y) reads
 // element 0 with this compiler, so vector elements go through this function.
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
 
-__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
-  return (float)__builtin_bit_cast(_Float16, h);
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
 }
 
-// ---------------------------------------------------------------- decoders
-// Each decoder fills z[24] (signed integer coordinates), cls and gain.
-
-// Magnitude of level code c in class record t (codes 0..7).
-__device__ __forceinline__ int mag_of(const DevClass& t, uint32_t lo, uint32_t hi, int code) {
-  return (int)(__builtin_amdgcn_perm(hi, lo, (uint32_t)code) & 0xFFu);
+// 4×4 bit transpose inside every nibble: on return n[r] bit (4g + q) is bit
+// (4g + r) of plane q (q = 0..3), i.e. nibble g of n[r] collects the four
+// plane bits of coordinate 4g + r.
+__device__ __forceinline__ void nibble_transpose(uint32_t q0, uint32_t q1, uint32_t q2,
+                                                 uint32_t q3, uint32_t n[4]) {
+  const uint32_t a0 = bfi(0xCCCCCCCCu, q2 << 2, q0);
+  const uint32_t a2 = bfi(0x33333333u, q0 >> 2, q2);
+  const uint32_t a1 = bfi(0xCCCCCCCCu, q3 << 2, q1);
+  const uint32_t a3 = bfi(0x33333333u, q1 >> 2, q3);
+  n[0] = bfi(0xAAAAAAAAu, a1 << 1, a0);
+  n[1] = bfi(0x55555555u, a0 >> 1, a1);
+  n[2] = bfi(0xAAAAAAAAu, a3 << 1, a2);
+  n[3] = bfi(0x55555555u, a2 >> 1, a3);
 }
 
-// Planes14 record at byte offset off of base: class [0,9) | gain 9 |
-// sign mask [10,34) | p0 [34,58) | p1 [58,82) | p2 [82,106).  The record
-// starts at 14·b ≡ 0 or 2 (mod 4): a four-word window read with a 0- or
-// 16-bit funnel shift (§2.3).
-__device__ __forceinline__ void decode_planes14(const uint8_t* base, uint64_t off,
-                                                const DevClass* tab, int* z, uint32_t& cls,
-                                                uint32_t& gain) {
-  u32x4 w = *(const u32x4*)(base + (off & ~3ull));
-  uint32_t sh = (uint32_t)(off & 2) * 8u;
-  uint32_t r0 = align(w.y, w.x, sh), r1 = align(w.z, w.y, sh), r2 = align(w.w, w.z, sh);
-  uint32_t r3 = w.w >> sh;
-  cls = r0 & 511u;
-  gain = (r0 >> 9) & 1u;
-  uint32_t sm = align(r1, r0, 10) & 0xFFFFFFu;
-  uint32_t p0 = (r1 >> 2) & 0xFFFFFFu;
-  uint32_t p1 = align(r2, r1, 26) & 0xFFFFFFu;
-  uint32_t p2 = align(r3, r2, 18) & 0xFFFFFFu;
-  const uint32_t* mw = (const uint32_t*)tab[cls].mag;
-  uint32_t lo = mw[0], hi = mw[1];
+// The three selector-source words of nibble register N: each holds the
+// nibbles of two coordinates in the low nibbles of bytes 0/1 and 2/3:
+//   s[0]: coordinates (r, 16+r)   s[1]: (4+r, 20+r)   s[2]: (8+r, 12+r)
+__device__ __forceinline__ void pair_sources(uint32_t N, uint32_t s[3]) {
+  const uint32_t R = align(N, N, 4);           // rotate right by one nibble
+  s[0] = perm(N, N, 0x02020000u);
+  s[1] = perm(R, R, 0x02020000u);
+  s[2] = perm(R, N, 0x05050101u);
+}
+
+// Planes core: nibble (c0, c1, c2, ¬s) per coordinate, with c = level + 1 the
+// level code -> 12 binary16 pairs.  Selector byte for the low half: the code
+// (table bytes 1..5 hold |z| of levels 0..4); for the high half: 0 (table
+// byte 0 = 0x80) when negative, 8 when not (v_perm's selector 8 replicates
+// bit 7 of table byte 1, a magnitude below 0x80, giving 0x00).  Pair 3r + k
+// of h[] covers the coordinates listed by pair_sources.
+__device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t sm,
+                                            uint32_t tlo, uint32_t thi, uint32_t h[12]) {
+  uint32_t n[4];
+  nibble_transpose(p0, p1, p2, ~sm, n);
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) {
-    int code = (int)((p0 >> i) & 1u) | (int)((p1 >> i) & 1u) << 1 | (int)((p2 >> i) & 1u) << 2;
-    int a = mag_of(tab[cls], lo, hi, code);
-    z[i] = ((sm >> i) & 1u) ? -a : a;
-  }
-}
-
-// Planes12x: 12-byte record class | gain | sign mask | p0 | p1 | exception
-// field [82,96); a nonzero field points into the tile's exception list of
-// exact Planes14 records (§3.2).
-__device__ __forceinline__ void decode_planes12x(const GemvArgs& a, uint64_t idx, int64_t tile,
-                                                 const DevClass* tab, int* z, uint32_t& cls,
-                                                 uint32_t& gain) {
-  u32x3 w = *(const u32x3*)(a.main + idx * kPlanes12Bytes);
-  uint32_t field = w.z >> kP12ExcShift;
-  if (field) {
-    uint32_t tb = ((const uint32_t*)a.side1)[tile];
-    decode_planes14(a.side0, (uint64_t)(tb + field - 1) * kPlanes14Bytes, tab, z, cls, gain);
-    return;
-  }
-  cls = w.x & 511u;
-  gain = (w.x >> 9) & 1u;
-  uint32_t sm = align(w.y, w.x, 10) & 0xFFFFFFu;
-  uint32_t p0 = (w.y >> 2) & 0xFFFFFFu;
-  uint32_t p1 = align(w.z, w.y, 26) & 0xFFFFFFu;
-  const uint32_t* mw = (const uint32_t*)tab[cls].mag;
-  uint32_t lo = mw[0], hi = mw[1];
+  for (int r = 0; r < 4; ++r) {
+    uint32_t s[3];
+    pair_sources(n[r], s);
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) {
-    int code = (int)((p0 >> i) & 1u) | (int)((p1 >> i) & 1u) << 1;
-    int m = mag_of(tab[cls], lo, hi, code);
-    z[i] = ((sm >> i) & 1u) ? -m : m;
+    for (int k = 0; k < 3; ++k) h[3 * r + k] = perm(thi, tlo, s[k] & 0x08070807u);
   }
 }
 
-// Slot32: 16- or 20-byte records located through the unit's side entry (u64
-// bitmap of 20-byte records, u32 word offset of the unit's first record); a
-// fixed five-word window; one-hot masks of levels 1..L−1 at [34 + 24(k−1), …).
-__device__ __forceinline__ void decode_slot32(const GemvArgs& a, int64_t unit, int lane,
-                                              const DevClass* tab, int* z, uint32_t& cls,
-                                              uint32_t& gain) {
-  const uint8_t* ent = a.side0 + unit * kUnitEntryBytes;
-  uint64_t bits = *(const uint64_t*)ent;
-  uint32_t base = *(const uint32_t*)(ent + 8);
-  uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << lane) - 1ull));
-  const uint32_t* rec = (const uint32_t*)(a.main + (uint64_t)base * 4 +
-                                          (uint64_t)lane * kSlot32Small +
-                                          (uint64_t)nbelow * (kSlot32Large - kSlot32Small));
-  uint32_t r0 = rec[0], r1 = rec[1], r2 = rec[2], r3 = rec[3], r4 = rec[4];
-  cls = r0 & 511u;
-  gain = (r0 >> 9) & 1u;
-  uint32_t L = tab[cls].info & 0xFFu;
-  uint32_t sm = align(r1, r0, 10) & 0xFFFFFFu;
-  uint32_t m1 = L > 1 ? (r1 >> 2) & 0xFFFFFFu : 0u;
-  uint32_t m2 = L > 2 ? align(r2, r1, 26) & 0xFFFFFFu : 0u;
-  uint32_t m3 = L > 3 ? align(r3, r2, 18) & 0xFFFFFFu : 0u;
-  uint32_t m4 = L > 4 ? align(r4, r3, 10) & 0xFFFFFFu : 0u;
-  const uint32_t* mw = (const uint32_t*)tab[cls].mag;
-  uint32_t lo = mw[0], hi = mw[1];
+// Golay70 core: nibble (c0, c1, side, 0) -> index side·4 + code; the low half
+// is |value| from one 8-byte table, the high half its sign byte from another.
+__device__ __forceinline__ void golay70_core(uint32_t c0, uint32_t c1, uint32_t side,
+                                             const G70Entry& t, uint32_t h[12]) {
+  uint32_t n[4];
+  nibble_transpose(c0, c1, side, 0u, n);
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) {
-    int code = (int)((m1 >> i) & 1u) + 2 * (int)((m2 >> i) & 1u) + 3 * (int)((m3 >> i) & 1u) +
-               4 * (int)((m4 >> i) & 1u);
-    int m = mag_of(tab[cls], lo, hi, code);
-    z[i] = ((sm >> i) & 1u) ? -m : m;
-  }
-}
-
-// Golay70: 9-byte record class | gain | 12-bit codeword rank | 24 two-bit
-// codes at [22,70) | exception flag 70.  The side of coordinate i is bit i of
-// the codeword; its value is the class's g70[side][code].  Exceptions are
-// exact Planes14 records located through the unit's side entry.
-__device__ __forceinline__ void decode_golay70(const GemvArgs& a, uint64_t idx, int64_t unit,
-                                               int lane, const DevClass* tab,
-                                               const uint32_t* cw, int* z, uint32_t& cls,
-                                               uint32_t& gain) {
-  uint64_t off = idx * kGolay70Bytes;
-  u32x3 w = *(const u32x3*)(a.main + (off & ~3ull));
-  uint32_t sh = (uint32_t)(off & 3) * 8u;
-  uint32_t r0 = align(w.y, w.x, sh), r1 = align(w.z, w.y, sh), r2 = w.z >> sh;
-  if ((r2 >> 6) & 1u) {
-    const uint8_t* ent = a.side1 + unit * kUnitEntryBytes;
-    uint64_t bits = *(const uint64_t*)ent;
-    uint32_t base = *(const uint32_t*)(ent + 8);
-    uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << lane) - 1ull));
-    decode_planes14(a.side0, (uint64_t)(base + nbelow) * kPlanes14Bytes, tab, z, cls, gain);
-    return;
-  }
-  cls = r0 & 511u;
-  gain = (r0 >> 9) & 1u;
-  uint32_t word = cw[(r0 >> 10) & 0xFFFu];
-  uint64_t codes = ((((uint64_t)r2 << 32) | r1) << 10) | (r0 >> 22);
-  const int8_t* v = &tab[cls].g70[0][0];
+  for (int r = 0; r < 4; ++r) {
+    uint32_t s[3];
+    pair_sources(n[r], s);
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) {
-    int side = (int)((word >> i) & 1u);
-    int code = (int)((codes >> (2 * i)) & 3u);
-    z[i] = v[side * 4 + code];
+    for (int k = 0; k < 3; ++k) {
+      const uint32_t sel = s[k] & 0x07070707u;
+      h[3 * r + k] = bfi(0xFF00FF00u, perm(t.shi, t.slo, sel), perm(t.ahi, t.alo, sel));
+    }
   }
 }
 
-// Decode the block at storage index idx of unit (tile, g), lane `lane`.
+// Coordinates of pair k of h[] (and of the staged x pairs).
+__device__ __forceinline__ void pair_coords(int k, int& c0, int& c1) {
+  const int r = k / 3, m = k % 3;
+  c0 = m == 0 ? r : (m == 1 ? 4 + r : 8 + r);
+  c1 = m == 0 ? 16 + r : (m == 1 ? 20 + r : 12 + r);
+}
+
+// ---------------------------------------------------------- per-block reads
+// Where a lane's block sits: storage index ubase + ul, with ubase the first
+// block of the unit (uniform across the wavefront) and ul the lane's position
+// inside the unit.
+struct LaneBlock {
+  int64_t ubase;     // storage index of the unit's first block (wave-uniform)
+  int32_t unit;      // tile·groups + g (wave-uniform)
+  int32_t tile;      // (wave-uniform)
+  uint32_t ul;       // position inside the unit
+  uint32_t loff;     // ul · record stride (fixed-stride layouts)
+  bool valid;
+  __device__ __forceinline__ uint64_t idx() const { return (uint64_t)ubase + ul; }
+};
+
+template <int LAYOUT> struct Stride { static constexpr uint32_t v = 0; };
+template <> struct Stride<LEECH_PLANES14> { static constexpr uint32_t v = kPlanes14Bytes; };
+template <> struct Stride<LEECH_PLANES12X> { static constexpr uint32_t v = kPlanes12Bytes; };
+template <> struct Stride<LEECH_GOLAY70> { static constexpr uint32_t v = kGolay70Bytes; };
+
+// Words a lane prefetches for one block.
+struct Pref {
+  uint32_t w0, w1, w2, w3, w4;
+  uint32_t scale;
+  uint32_t sh;       // bit offset of the record inside its first word
+};
+
+// Window of n words holding the record of block i at stride `stride` bytes:
+// the wave-uniform part of the byte offset goes into the base pointer, the
+// lane part stays a 32-bit offset.
+template <int STRIDE>
+__device__ __forceinline__ const uint32_t* record_window(const uint8_t* base, const LaneBlock& b,
+                                                         uint32_t& sh) {
+  const uint64_t U = (uint64_t)b.ubase * STRIDE;
+  const uint32_t lo = (uint32_t)(U & 3u) + b.loff;
+  sh = (lo & 3u) * 8u;
+  return (const uint32_t*)(base + (U & ~3ull) + (lo & ~3u));
+}
+
+// Loads are issued unconditionally (callers hand in a clamped, in-bounds
+// block for lanes or units that do not exist and ignore the data): branches
+// around loads would make the compiler's wait counts conservative.
 template <int LAYOUT>
-__device__ __forceinline__ void decode_block(const GemvArgs& a, uint64_t idx, int64_t tile,
-                                             int64_t unit, int lane, const DevClass* tab,
-                                             const uint32_t* cw, int* z, uint32_t& cls,
-                                             uint32_t& gain) {
-  if constexpr (LAYOUT == LEECH_PLANES14)
-    decode_planes14(a.main, idx * kPlanes14Bytes, tab, z, cls, gain);
-  else if constexpr (LAYOUT == LEECH_PLANES12X)
-    decode_planes12x(a, idx, tile, tab, z, cls, gain);
-  else if constexpr (LAYOUT == LEECH_SLOT32)
-    decode_slot32(a, unit, lane, tab, z, cls, gain);
-  else
-    decode_golay70(a, idx, unit, lane, tab, cw, z, cls, gain);
+__device__ __forceinline__ Pref load_block(const GemvArgs& a, const LaneBlock& b) {
+  Pref p = {0, 0, 0, 0, 0, 0, 0};
+  if constexpr (LAYOUT == LEECH_PLANES14) {
+    const u32x4 w = *(const u32x4*)record_window<kPlanes14Bytes>(a.main, b, p.sh);
+    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w;
+  } else if constexpr (LAYOUT == LEECH_PLANES12X) {
+    const u32x3 w = *(const u32x3*)record_window<kPlanes12Bytes>(a.main, b, p.sh);
+    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
+  } else if constexpr (LAYOUT == LEECH_SLOT32) {
+    const uint8_t* ent = a.side0 + b.unit * kUnitEntryBytes;
+    const uint64_t bits = *(const uint64_t*)ent;
+    const uint32_t base = *(const uint32_t*)(ent + 8);
+    const uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << b.ul) - 1ull));
+    const uint32_t* rec = (const uint32_t*)(a.main + (uint64_t)base * 4) +
+                          (b.ul * (uint32_t)kSlot32Small + nbelow * (uint32_t)(kSlot32Large - kSlot32Small)) / 4;
+    const u32x4 w = *(const u32x4*)rec;
+    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w; p.w4 = rec[4];
+  } else if constexpr (LAYOUT == LEECH_GOLAY70) {
+    const u32x3 w = *(const u32x3*)record_window<kGolay70Bytes>(a.main, b, p.sh);
+    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
+  }
+  if constexpr (LAYOUT != kNoWeights)
+    p.scale = *(const uint16_t*)((const uint8_t*)(a.scale + b.ubase) + (uint32_t)(b.ul * 2u));
+  return p;
+}
+
+// Planes14 fields of the four-word window starting at byte (14·i) & ~3: the
+// record begins 0 or 16 bits in (§2.3: a four-word window, shift 0 or 16).
+__device__ __forceinline__ void planes14_fields(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
+                                                uint32_t sh, uint32_t& e, uint32_t& p0,
+                                                uint32_t& p1, uint32_t& p2, uint32_t& sm) {
+  const uint32_t r0 = align(w1, w0, sh), r1 = align(w2, w1, sh), r2 = align(w3, w2, sh);
+  const uint32_t r3 = w3 >> sh;
+  e = r0 & 1023u;              // class | gain << 9
+  sm = align(r1, r0, 10);      // plane bits above 23 are never read
+  p0 = r1 >> 2;
+  p1 = align(r2, r1, 26);
+  p2 = align(r3, r2, 18);
+}
+
+// Decode one block into 12 binary16 pairs and its table entry index.
+// tab(e) returns the LdsEntry of e and g70(class) the G70Entry of a class
+// (from LDS in the GEMV, built from the global table in the verification
+// decode); cw(rank) is the Golay codeword of a rank.
+template <int LAYOUT, class TAB, class G70, class CW>
+__device__ __forceinline__ void decode_block(const GemvArgs& a, const LaneBlock& b, const Pref& p,
+                                             TAB tab, G70 g70, CW cw, uint32_t h[12], uint32_t& e) {
+  uint32_t p0 = 0, p1 = 0, p2 = 0, sm = 0;
+  if constexpr (LAYOUT == LEECH_PLANES14) {
+    planes14_fields(p.w0, p.w1, p.w2, p.w3, p.sh, e, p0, p1, p2, sm);
+  } else if constexpr (LAYOUT == LEECH_PLANES12X) {
+    const uint32_t field = p.w2 >> kP12ExcShift;
+    if (field) {      // five-level block: exact Planes14 record from the tile's list
+      const uint64_t ex = (uint64_t)(((const uint32_t*)a.side1)[b.tile] + field - 1);
+      const u32x4 w = *(const u32x4*)(a.side0 + ((ex * kPlanes14Bytes) & ~3ull));
+      planes14_fields(w.x, w.y, w.z, w.w, (uint32_t)(ex & 1) * 16u, e, p0, p1, p2, sm);
+    } else {
+      // two-plane level (0..3) -> code planes of level + 1, bit-parallel
+      e = p.w0 & 1023u;
+      sm = align(p.w1, p.w0, 10);
+      const uint32_t l0 = p.w1 >> 2, l1 = align(p.w2, p.w1, 26);
+      p0 = ~l0;
+      p1 = l0 ^ l1;
+      p2 = l0 & l1;
+    }
+  } else if constexpr (LAYOUT == LEECH_SLOT32) {
+    // one-hot masks of levels 1..4 -> code planes of level + 1 (codes 1..5)
+    e = p.w0 & 1023u;
+    const uint32_t L = tab(e).nlev;
+    sm = align(p.w1, p.w0, 10);
+    const uint32_t m1 = L > 1 ? p.w1 >> 2 : 0u;
+    const uint32_t m2 = L > 2 ? align(p.w2, p.w1, 26) : 0u;
+    const uint32_t m3 = L > 3 ? align(p.w3, p.w2, 18) : 0u;
+    const uint32_t m4 = L > 4 ? align(p.w4, p.w3, 10) : 0u;
+    p0 = ~(m1 | m3);
+    p1 = m1 | m2;
+    p2 = m3 | m4;
+  } else if constexpr (LAYOUT == LEECH_GOLAY70) {
+    const uint32_t r0 = align(p.w1, p.w0, p.sh), r1 = align(p.w2, p.w1, p.sh), r2 = p.w2 >> p.sh;
+    if ((r2 >> 6) & 1u) {   // exception: exact Planes14 record located by the unit entry
+      const uint8_t* ent = a.side1 + b.unit * kUnitEntryBytes;
+      const uint64_t bits = *(const uint64_t*)ent;
+      const uint32_t base = *(const uint32_t*)(ent + 8);
+      const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << b.ul) - 1ull));
+      const u32x4 w = *(const u32x4*)(a.side0 + ((ex * kPlanes14Bytes) & ~3ull));
+      planes14_fields(w.x, w.y, w.z, w.w, (uint32_t)(ex & 1) * 16u, e, p0, p1, p2, sm);
+    } else {
+      e = r0 & 1023u;
+      const uint32_t side = cw((r0 >> 10) & 0xFFFu);
+      golay70_core(align(r1, r0, 22), align(r2, r1, 14), side, g70(e & 511u), h);
+      return;
+    }
+  }
+  const LdsEntry t = tab(e);
+  planes_core(p0, p1, p2, sm, t.tlo, t.thi, h);
+}
+
+__device__ __forceinline__ LaneBlock lane_block(const GemvArgs& a, int64_t tile, int R_t, int64_t g,
+                                                int rl, int cl) {
+  LaneBlock b;
+  const int C_g = (int)min((int64_t)a.C, a.nb - g * a.C);
+  b.valid = rl < R_t && cl < C_g;
+  b.ul = (uint32_t)(rl * C_g + cl);
+  b.loff = b.ul * Stride<LEECH_PLANES14>::v;   // overwritten per layout by the caller
+  b.tile = (int32_t)tile;
+  b.unit = (int32_t)(tile * a.groups + g);
+  b.ubase = tile * a.R * a.nb + g * R_t * a.C;
+  return b;
+}
+
+// The LDS entries, built from the device table: one 16-byte load per entry.
+__device__ __forceinline__ LdsEntry make_entry(const DevClass* tab, uint32_t e, float cen0,
+                                               float cen1) {
+  const u32x4a d = *(const u32x4a*)&tab[e & 511u];      // perm[8], inv_norm, info
+  LdsEntry t;
+  t.tlo = d.x;
+  t.thi = d.y;
+  t.factor = __builtin_bit_cast(float, (uint32_t)d.z) * ((e >> 9) ? cen1 : cen0) * kTwo24;
+  t.nlev = d.w & 0xFFu;
+  return t;
+}
+
+__device__ __forceinline__ G70Entry make_g70(const DevClass* tab, uint32_t c) {
+  const u32x4a d = *(const u32x4a*)&tab[c];
+  const u32x4a v = *((const u32x4a*)&tab[c] + 1);        // g70[8], g70abs[8]
+  G70Entry t;
+  t.alo = v.z;
+  t.ahi = v.w;
+  const uint32_t sg = (uint32_t)d.w >> 24;
+  uint32_t slo = 0, shi = 0;
+  for (int k = 0; k < 4; ++k) {
+    slo |= ((sg >> k) & 1u) << (8 * k + 7);
+    shi |= ((sg >> (k + 4)) & 1u) << (8 * k + 7);
+  }
+  t.slo = slo;
+  t.shi = shi;
+  return t;
+}
+
+// x of block j in the cores' pair order: three 16-byte loads, then pair k
+// (coordinates pair_coords(k)) picked by one v_perm_b32 each.
+struct XBlock {
+  u32x4a v0, v1, v2;
+};
+__device__ __forceinline__ XBlock load_x_block(const uint16_t* xj) {
+  const u32x4a* src = (const u32x4a*)xj;
+  return XBlock{src[0], src[1], src[2]};
+}
+__device__ __forceinline__ void store_x_block(const XBlock& xb, uint32_t* dst) {
+  const uint32_t w[12] = {xb.v0.x, xb.v0.y, xb.v0.z, xb.v0.w, xb.v1.x, xb.v1.y,
+                          xb.v1.z, xb.v1.w, xb.v2.x, xb.v2.y, xb.v2.z, xb.v2.w};
+  uint32_t o[12];
+#pragma unroll
+  for (int k = 0; k < 12; ++k) {
+    int c0, c1;
+    pair_coords(k, c0, c1);
+    // low half: half c0 % 2 of word c0 / 2 (selector bytes 0..3 pick S1);
+    // high half: half c1 % 2 of word c1 / 2 (bytes 4..7 pick S0)
+    const uint32_t sel = (c0 & 1 ? 0x0302u : 0x0100u) | (c1 & 1 ? 0x07060000u : 0x05040000u);
+    o[k] = perm(w[c1 >> 1], w[c0 >> 1], sel);
+  }
+  u32x4a* d = (u32x4a*)dst;
+  d[0] = u32x4a{o[0], o[1], o[2], o[3]};
+  d[1] = u32x4a{o[4], o[5], o[6], o[7]};
+  d[2] = u32x4a{o[8], o[9], o[10], o[11]};
 }
 
 // ------------------------------------------------------------------- GEMV
 template <int LAYOUT>
 __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  const int64_t Kpad = a.nb * kDim;
-  uint16_t* xs = (uint16_t*)smem;                                  // Kpad halves
-  const size_t xbytes = ((size_t)Kpad * 2 + 15) & ~(size_t)15;
-  DevClass* ts = (DevClass*)(smem + xbytes);                        // 512 records
-  const size_t tbytes = (LAYOUT == kNoWeights) ? 0 : LEECH_DEVICE_TABLE_BYTES;
-  uint32_t* cws = (uint32_t*)(smem + xbytes + tbytes);               // Golay70: 4096 words
-  const size_t cbytes = (LAYOUT == LEECH_GOLAY70) ? 4096 * 4 : 0;
-  float* red = (float*)(smem + xbytes + tbytes + cbytes);          // waves × 64
+  const int64_t nb = a.nb;
+  uint32_t* xs = (uint32_t*)smem;                                   // nb × 12 x pairs
+  const size_t xbytes = (size_t)nb * 48;
+  LdsEntry* ts = (LdsEntry*)(smem + xbytes);                         // 1024 entries
+  const size_t tbytes = (LAYOUT == kNoWeights) ? 0 : 1024 * sizeof(LdsEntry);
+  G70Entry* gs = (G70Entry*)(smem + xbytes + tbytes);                // Golay70: 512 entries
+  uint32_t* cws = (uint32_t*)(smem + xbytes + tbytes + 512 * sizeof(G70Entry));  // 4096 words
+  const size_t gbytes = (LAYOUT == LEECH_GOLAY70) ? 512 * sizeof(G70Entry) + 4096 * 4 : 0;
+  float* red = (float*)(smem + xbytes + tbytes + gbytes);          // waves × 64
 
-  const int tid = threadIdx.x;
-  const int nthr = blockDim.x;
-  {  // stage x, the class table (and the codeword table) into LDS
-    const u32x4a* src = (const u32x4a*)a.x;
-    u32x4a* dst = (u32x4a*)xs;
-    for (int64_t k = tid; k < Kpad / 8; k += nthr) dst[k] = src[k];
-    if (LAYOUT != kNoWeights) {
-      const u32x4a* ts_src = (const u32x4a*)a.table;
-      for (int k = tid; k < LEECH_DEVICE_TABLE_BYTES / 16; k += nthr) ((u32x4a*)ts)[k] = ts_src[k];
-    }
-    if (LAYOUT == LEECH_GOLAY70) {
-      const u32x4a* c_src = (const u32x4a*)a.codewords;
-      for (int k = tid; k < 4096 / 4; k += nthr) ((u32x4a*)cws)[k] = c_src[k];
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int tile = (int)blockIdx.x;
+  const int R_t = (int)min((int64_t)a.R, a.M - (int64_t)tile * a.R);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int rl = lane / a.C, cl = lane % a.C;
+  const int groups = (int)a.groups, waves = a.waves;     // unit counts fit 32 bits
+  // lane constants: position inside a full unit and inside the narrower last
+  // one; a lane with no block there takes block 0 (in bounds) and is masked
+  const int C_last = (int)(a.nb - (int64_t)(groups - 1) * a.C);
+  const bool row_ok = rl < R_t, last_ok = row_ok && cl < C_last;
+  const uint32_t ul_f = row_ok ? (uint32_t)(rl * a.C + cl) : 0u;
+  const uint32_t ul_l = last_ok ? (uint32_t)(rl * C_last + cl) : 0u;
+  const uint32_t lo_f = ul_f * Stride<LAYOUT>::v, lo_l = ul_l * Stride<LAYOUT>::v;
+  const int64_t tile_base = (int64_t)tile * a.R * a.nb;
+  // the block of this lane in unit g (g wave-uniform); past the last unit an
+  // in-bounds stand-in with valid = false
+  auto unit_block = [&](int g) -> LaneBlock {
+    LaneBlock b;
+    const bool beyond = g >= groups;
+    g = beyond ? groups - 1 : g;
+    const bool last = g == groups - 1;
+    b.valid = !beyond && (last ? last_ok : row_ok);
+    b.ul = last ? ul_l : ul_f;
+    b.loff = last ? lo_l : lo_f;
+    b.tile = tile;
+    b.unit = tile * groups + g;
+    b.ubase = tile_base + (int64_t)g * (R_t * a.C);
+    return b;
+  };
+
+  // Prologue, ordered for the in-order load counter: first the L2-resident
+  // staging loads (x blocks, class table), then the units' record loads, then
+  // the LDS writes, which wait only for the older staging loads.
+  constexpr int kXPer = 2, kTPer = 2;          // staged items per thread held in registers
+  // rare overflow first (nb > kXPer·threads, or fewer threads than table
+  // entries / kTPer): loads of unknown count here, before the ordered ones
+  for (int64_t j = tid + (int64_t)kXPer * nthr; j < nb; j += nthr)
+    store_x_block(load_x_block(a.x + 24 * j), xs + 12 * j);
+  if constexpr (LAYOUT != kNoWeights)
+    for (int e = tid + kTPer * nthr; e < 1024; e += nthr)
+      ts[e] = make_entry(a.table, (uint32_t)e, a.cen0, a.cen1);
+  if constexpr (LAYOUT == LEECH_GOLAY70) {
+    for (int c = tid; c < 512; c += nthr) gs[c] = make_g70(a.table, (uint32_t)c);
+    for (int k = tid; k < 1024; k += nthr) ((u32x4a*)cws)[k] = ((const u32x4a*)a.codewords)[k];
+  }
+  XBlock xr[kXPer];
+#pragma unroll
+  for (int q = 0; q < kXPer; ++q) {
+    const int64_t j = min(tid + (int64_t)q * nthr, nb - 1);    // clamped: loads stay unconditional
+    xr[q] = load_x_block(a.x + 24 * j);
+  }
+  u32x4a tr[kTPer];
+  if constexpr (LAYOUT != kNoWeights) {
+#pragma unroll
+    for (int q = 0; q < kTPer; ++q) tr[q] = *(const u32x4a*)&a.table[(tid + q * nthr) & 511];
+  }
+  Pref pf[kPrefetch];
+#pragma unroll
+  for (int d = 0; d < kPrefetch; ++d) {
+    pf[d] = load_block<LAYOUT>(a, unit_block(wave + d * waves));
+    __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
+  }
+#pragma unroll
+  for (int q = 0; q < kXPer; ++q) {
+    const int64_t j = tid + (int64_t)q * nthr;
+    if (j < nb) store_x_block(xr[q], xs + 12 * j);
+  }
+  if constexpr (LAYOUT != kNoWeights) {
+#pragma unroll
+    for (int q = 0; q < kTPer; ++q) {
+      const int e = tid + q * nthr;
+      if (e < 1024) {
+        LdsEntry t;
+        t.tlo = tr[q].x;
+        t.thi = tr[q].y;
+        t.factor = __builtin_bit_cast(float, (uint32_t)tr[q].z) * ((e >> 9) ? a.cen1 : a.cen0) * kTwo24;
+        t.nlev = tr[q].w & 0xFFu;
+        ts[e] = t;
+      }
     }
   }
   __syncthreads();
 
-  const int64_t tile = blockIdx.x;
-  const int R = a.R, C = a.C;
-  const int R_t = (int)min((int64_t)R, a.M - tile * R);
-  const int wave = tid >> 6, lane = tid & 63;
-  const int rl = lane / C, cl = lane % C;
+  auto tab = [&](uint32_t e) -> LdsEntry { return ts[e]; };
+  auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
+  auto cw = [&](uint32_t r) -> uint32_t { return cws[r]; };
   float acc = 0.0f;
-
-  for (int64_t g = wave; g < a.groups; g += a.waves) {
-    const int C_g = (int)min((int64_t)C, a.nb - g * C);
-    if (rl < R_t && cl < C_g) {
-      const int ul = rl * C_g + cl;                    // lane inside the unit
-      const uint64_t idx = (uint64_t)(tile * R * a.nb + g * R_t * C + ul);
-      const int64_t j = g * C + cl;
-      int z[kDim];
-      uint32_t cls = 0, gain = 0;
-      float f;
-      if constexpr (LAYOUT == kNoWeights) {
+  // One unit: decode slot pf[d] for unit g and accumulate.
+  // Lanes without a block decode their in-bounds stand-in and add 0.
+  auto process = [&](const Pref& p, int g) {
+    const LaneBlock b = unit_block(g);
+    const int j = g * a.C + (b.valid ? cl : 0);
+    const u32x4a* xp = (const u32x4a*)(xs + 12 * j);
+    const u32x4a x0 = xp[0], x1 = xp[1], x2 = xp[2];
+    const uint32_t xw[12] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w,
+                             x2.x, x2.y, x2.z, x2.w};
+    if constexpr (LAYOUT == kNoWeights) {
+      float s = 0.0f;
 #pragma unroll
-        for (int i = 0; i < kDim; ++i) z[i] = 1;
-        f = 1.0f;
-      } else {
-        decode_block<LAYOUT>(a, idx, tile, tile * a.groups + g, ul, ts, cws, z, cls, gain);
-        const float s = half_bits_to_float(a.scale[idx]);
-        f = (s * (gain ? a.cen1 : a.cen0)) * ts[cls].inv_norm;
-      }
-      const half2_t* xp = (const half2_t*)(xs + 24 * j);
-      float s0 = 0.0f;
+      for (int k = 0; k < 12; ++k) s = __builtin_amdgcn_fdot2(as_h2(0x3C003C00u), as_h2(xw[k]), s, false);
+      acc += b.valid ? s : 0.0f;
+    } else {
+      uint32_t h[12], e;
+      decode_block<LAYOUT>(a, b, p, tab, g70, cw, h, e);
+      float s = 0.0f;
 #pragma unroll
-      for (int k = 0; k < 12; ++k) s0 = __builtin_amdgcn_fdot2(pack2(z[2 * k], z[2 * k + 1]), xp[k], s0, false);
-      acc = __builtin_fmaf(s0, f, acc);
+      for (int k = 0; k < 12; ++k) s = __builtin_amdgcn_fdot2(as_h2(h[k]), as_h2(xw[k]), s, false);
+      const float f = half_bits_to_float(p.scale) * ts[e].factor;
+      acc = __builtin_fmaf(s, b.valid ? f : 0.0f, acc);
+    }
+  };
+  const int units = (groups - wave + waves - 1) / waves;   // this wave's units
+  int done = 0;
+  // Full rounds: consume every slot, refilling each with the unit kPrefetch
+  // steps ahead (past the wave's last unit the refill is an in-bounds
+  // stand-in).  Decoding before refilling lets the refill reuse the slot's
+  // registers: a refill into fresh registers would be moved back at the loop
+  // latch, and moving a register with a load in flight waits for every
+  // outstanding load.
+  for (; units - done > kPrefetch; done += kPrefetch) {
+#pragma unroll
+    for (int d = 0; d < kPrefetch; ++d) {
+      const int g = wave + (done + d) * waves;
+      process(pf[d], g);
+      pf[d] = load_block<LAYOUT>(a, unit_block(g + kPrefetch * waves));
     }
   }
-  for (int off = 1; off < C; off <<= 1) acc += __shfl_xor(acc, off);
+  // the last ≤ kPrefetch units are in flight: straight-line, no refills
+#pragma unroll
+  for (int d = 0; d < kPrefetch; ++d)
+    if (d < units - done) process(pf[d], wave + (done + d) * waves);
+  for (int off = 1; off < a.C; off <<= 1) acc += __shfl_xor(acc, off);
   if (cl == 0 && rl < R_t) red[wave * 64 + rl] = acc;
   __syncthreads();
   if (tid < R_t) {
     float y = 0.0f;
     for (int w = 0; w < a.waves; ++w) y += red[w * 64 + tid];
-    a.y[tile * R + tid] = y;
+    a.y[(int64_t)tile * a.R + tid] = y;
   }
 }
 
 // --------------------------------------------------------- decode export
+// One thread per block, with the GEMV's own load and decode functions; the
+// binary16 pairs are turned back into integer coordinates (|z| in the low
+// byte of each half, the sign in its bit 15).
 template <int LAYOUT>
 __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, uint16_t* cout,
                                                      uint8_t* gout) {
-  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= a.M * a.nb) return;
-  const int64_t r = b / a.nb, j = b % a.nb;
+  const int64_t bi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (bi >= a.M * a.nb) return;
+  const int64_t r = bi / a.nb, j = bi % a.nb;
   const int64_t tile = r / a.R, g = j / a.C;
-  const int rl = (int)(r % a.R), cl = (int)(j % a.C);
   const int R_t = (int)min((int64_t)a.R, a.M - tile * a.R);
-  const int C_g = (int)min((int64_t)a.C, a.nb - g * a.C);
-  const int ul = rl * C_g + cl;
-  const uint64_t idx = (uint64_t)(tile * a.R * a.nb + g * R_t * a.C + ul);
-  int z[kDim];
-  uint32_t cls = 0, gain = 0;
-  decode_block<LAYOUT>(a, idx, tile, tile * a.groups + g, ul, a.table, a.codewords, z, cls,
-                       gain);
+  LaneBlock b = lane_block(a, tile, R_t, g, (int)(r % a.R), (int)(j % a.C));
+  b.loff = b.ul * Stride<LAYOUT>::v;
+  const Pref p = load_block<LAYOUT>(a, b);
+  auto tab = [&](uint32_t e) -> LdsEntry { return make_entry(a.table, e, 1.0f, 1.0f); };
+  auto g70 = [&](uint32_t c) -> G70Entry { return make_g70(a.table, c); };
+  auto cw = [&](uint32_t rk) -> uint32_t { return a.codewords[rk]; };
+  uint32_t h[12], e;
+  decode_block<LAYOUT>(a, b, p, tab, g70, cw, h, e);
+  int8_t z[kDim];
+#pragma unroll
+  for (int k = 0; k < 12; ++k) {
+    int c0, c1;
+    pair_coords(k, c0, c1);
+    const int m0 = (int)(h[k] & 0xFFu), m1 = (int)((h[k] >> 16) & 0xFFu);
+    z[c0] = (int8_t)(((h[k] >> 15) & 1u) ? -m0 : m0);
+    z[c1] = (int8_t)(((h[k] >> 31) & 1u) ? -m1 : m1);
+  }
   if (zout) {
-    uint32_t* zo = (uint32_t*)(zout + b * kDim);
+    uint32_t* zo = (uint32_t*)(zout + bi * kDim);
 #pragma unroll
     for (int q = 0; q < 6; ++q)
       zo[q] = (uint32_t)(uint8_t)z[4 * q] | (uint32_t)(uint8_t)z[4 * q + 1] << 8 |
               (uint32_t)(uint8_t)z[4 * q + 2] << 16 | (uint32_t)(uint8_t)z[4 * q + 3] << 24;
   }
-  if (cout) cout[b] = (uint16_t)cls;
-  if (gout) gout[b] = (uint8_t)gain;
+  if (cout) cout[bi] = (uint16_t)(e & 511u);
+  if (gout) gout[bi] = (uint8_t)(e >> 9);
 }
 
 // ------------------------------------------------------ FP16 GEMV control
@@ -350,7 +600,17 @@ static int hip_fail(const char* what, hipError_t e) {
   return set_error(LEECH_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-static int waves_for(int64_t groups) { return (int)std::max<int64_t>(1, std::min<int64_t>(8, groups)); }
+// Waves per workgroup: each wave walks every waves-th unit of the tile.  The
+// summation order depends on it, so it is a function of the shape only (the
+// LEECH_WAVES environment variable overrides the cap, for tuning).
+static int waves_for(int64_t groups) {
+  static const int cap = [] {
+    const char* v = std::getenv("LEECH_WAVES");
+    const int w = v ? std::atoi(v) : 0;
+    return (w >= 1 && w <= 16) ? w : 8;
+  }();
+  return (int)std::max<int64_t>(1, std::min<int64_t>(cap, groups));
+}
 
 static int check_desc_device(const leech_layout_desc* d) {
   if (!d) return set_error(LEECH_E_ARG, "desc is NULL");
@@ -374,10 +634,15 @@ static GemvArgs make_args(const leech_layout_desc* d) {
 }
 
 template <int LAYOUT>
+static size_t gemv_lds_bytes(const GemvArgs& a) {
+  return (size_t)a.nb * 48 + (LAYOUT == kNoWeights ? 0 : 1024 * sizeof(LdsEntry)) +
+         (LAYOUT == LEECH_GOLAY70 ? 512 * sizeof(G70Entry) + 4096 * 4 : 0) +
+         (size_t)a.waves * 64 * 4;
+}
+
+template <int LAYOUT>
 static int launch_gemv(const GemvArgs& a, hipStream_t st) {
-  size_t xbytes = ((size_t)a.nb * kDim * 2 + 15) & ~(size_t)15;
-  size_t shmem = xbytes + (LAYOUT == kNoWeights ? 0 : LEECH_DEVICE_TABLE_BYTES) +
-                 (LAYOUT == LEECH_GOLAY70 ? 4096 * 4 : 0) + (size_t)a.waves * 64 * 4;
+  const size_t shmem = gemv_lds_bytes<LAYOUT>(a);
   if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
   if (shmem > 64 * 1024) {
@@ -385,7 +650,7 @@ static int launch_gemv(const GemvArgs& a, hipStream_t st) {
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  int64_t tiles = (a.M + a.R - 1) / a.R;
+  const int64_t tiles = (a.M + a.R - 1) / a.R;
   hipLaunchKernelGGL(gemv_kernel<LAYOUT>, dim3((unsigned)tiles), dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
@@ -394,7 +659,7 @@ static int launch_gemv(const GemvArgs& a, hipStream_t st) {
 
 template <int LAYOUT>
 static int launch_decode(const GemvArgs& a, int8_t* z, uint16_t* c, uint8_t* g, hipStream_t st) {
-  int64_t n = a.M * a.nb;
+  const int64_t n = a.M * a.nb;
   hipLaunchKernelGGL(decode_kernel<LAYOUT>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                      a, z, c, g);
   hipError_t e = hipGetLastError();

@@ -8,6 +8,11 @@
 
 #include "leech.h"
 
+#ifndef __HIPCC__
+#define __host__
+#define __device__
+#endif
+
 namespace leech {
 
 constexpr int kDim = 24;
@@ -30,18 +35,23 @@ constexpr int kP12ExcShift = 82 - 64;          // bit position inside word 2
 constexpr uint32_t kP12ExcMax = (1u << 14) - 2; // largest storable local index
 
 // Device class record: 32 bytes per class id (LEECH_DEVICE_TABLE_BYTES / 512).
-//   mag[8]      : |z| of each level code 0..7 (codes ≥ n_levels are 0)
-//   inv_norm    : f32 of 1 / (4 √m)
-//   info        : n_levels | parity << 8 | shell << 16
-//   g70[2][4]   : Golay70 signed values, [side][2-bit code]
-//   reserved[8] : zero
+//   perm[8]   : byte table read by v_perm_b32: perm[0] = 0x80 (the binary16
+//               sign byte), perm[1 + k] = |z| of level k (k < n_levels),
+//               then zeros.  Planes records code level k as k + 1.
+//   inv_norm  : f32 of 1 / (4 √m)
+//   info      : n_levels | parity << 8 | shell << 16 | Golay70 sign bits << 24
+//               (bit side·4 + code set when g70[side][code] < 0)
+//   g70[2][4] : Golay70 signed values, [side][2-bit code]
+//   g70abs[8] : |g70[side][code]| at side·4 + code
 struct DevClass {
-  uint8_t mag[8];
+  uint8_t perm[8];
   float inv_norm;
   uint32_t info;
   int8_t g70[2][4];
-  uint8_t reserved[8];
+  uint8_t g70abs[8];
 };
+constexpr int kSignByteCode = 0;
+__host__ __device__ inline int level_code(int level) { return level + 1; }
 static_assert(sizeof(DevClass) == 32, "device class record is 32 bytes");
 
 // Geometry shared by the expansion and the kernels: rows are grouped into

@@ -171,3 +171,28 @@ def test_noweights_control(dev, dcb, M, K):
     scale = np.abs(inp.x.astype(np.float64)).sum()
     assert np.all(np.abs(y - want) <= 1e-5 * scale)
     assert np.all(y == y[0])              # the same sum in every row
+
+
+def test_graph_replays_match_eager(dev, dcb):
+    """A GEMV captured in a HIP graph gives the eager result on every replay,
+    with eager work and synchronisations between the replays."""
+    inp, (cls, sm, lv) = case(768, 1536, 1)
+    mats = {n: P.LeechMatrix.from_fields(dcb, lay, cls, inp.gain, sm, lv, inp.scale, dev)
+            for n, lay in P.LAYOUTS.items()}
+    x = torch.from_numpy(inp.x).to(dev)
+    eager = {n: m.gemv(x, centroids=CEN).clone() for n, m in mats.items()}
+    ys = {n: torch.zeros(768, dtype=torch.float32, device=dev) for n in mats}
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for n, m in mats.items():
+            m.gemv(x, ys[n], centroids=CEN)
+    for rep in range(4):
+        for y in ys.values():
+            y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for n in mats:
+            assert torch.equal(ys[n], eager[n]), (rep, n)
+        mats["planes14"].gemv(x, centroids=CEN)          # eager work between replays
+        torch.cuda.synchronize()
