@@ -60,7 +60,67 @@ struct GemvArgs {
   float cen0, cen1;
   int64_t M, nb, groups;
   int C, R, waves;
+  int64_t tiles;
+  uint64_t n_exc;               // exception records (Planes12x, Golay70)
 };
+
+// Waves per GEMV workgroup, at most: 8 waves leave each lane up to 256 VGPRs,
+// so the eight prefetch slots and the exception-path decode stay in registers.
+constexpr int kMaxWaves = 8;
+constexpr int kExcLdsBytes = 32 * 1024;   // a tile's exception records staged in LDS
+
+// Where side data comes from: global memory (verification decode, and the
+// GEMV's first prefetches) or the workgroup's LDS copies (the GEMV's loop).
+struct GlobalSide {
+  const GemvArgs* a;
+  __device__ __forceinline__ uint32_t p12_base(int tile) const {
+    return ((const uint32_t*)a->side1)[tile];
+  }
+  __device__ __forceinline__ void unit_entry(const uint8_t* side, int unit, uint64_t& bits,
+                                             uint32_t& base) const {
+    const uint8_t* ent = side + (int64_t)unit * kUnitEntryBytes;
+    bits = *(const uint64_t*)ent;
+    base = *(const uint32_t*)(ent + 8);
+  }
+  // four-word window holding exception record ex (exact Planes14 record)
+  __device__ __forceinline__ void exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const;
+};
+struct LdsSide {
+  const GemvArgs* a;
+  const uint8_t* exc;        // LDS copy of exception bytes from global offset exc_start
+  uint64_t exc_start;
+  bool exc_in_lds;           // false: the tile's records exceed the LDS budget
+  const uint8_t* units;      // LDS copy of the tile's unit entries
+  int unit0;                 // first unit id of the tile
+  uint32_t p12base;          // Planes12x: first exception index of the tile
+  __device__ __forceinline__ uint32_t p12_base(int) const { return p12base; }
+  __device__ __forceinline__ void unit_entry(const uint8_t*, int unit, uint64_t& bits,
+                                             uint32_t& base) const {
+    const uint8_t* ent = units + (unit - unit0) * kUnitEntryBytes;
+    bits = *(const uint64_t*)ent;
+    base = *(const uint32_t*)(ent + 8);
+  }
+  __device__ __forceinline__ void exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const;
+};
+
+__device__ __forceinline__ void GlobalSide::exc_window(uint64_t ex, uint32_t w[4],
+                                                      uint32_t& sh) const {
+  const uint64_t off = ex * kPlanes14Bytes;
+  const uint32_t* p = (const uint32_t*)(a->side0 + (off & ~3ull));
+  w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
+  sh = (uint32_t)(off & 2) * 8u;
+}
+__device__ __forceinline__ void LdsSide::exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const {
+  const uint64_t goff = ex * kPlanes14Bytes;
+  if (exc_in_lds) {
+    const uint32_t* p = (const uint32_t*)(exc + ((uint32_t)(goff - exc_start) & ~3u));
+    w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
+  } else {
+    const uint32_t* p = (const uint32_t*)(a->side0 + (goff & ~3ull));
+    w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
+  }
+  sh = (uint32_t)(goff & 2) * 8u;
+}
 
 // Per-(class, gain) entry staged in LDS; e = class | gain << 9.
 struct LdsEntry {
@@ -202,8 +262,8 @@ __device__ __forceinline__ const uint32_t* record_window(const uint8_t* base, co
 // Loads are issued unconditionally (callers hand in a clamped, in-bounds
 // block for lanes or units that do not exist and ignore the data): branches
 // around loads would make the compiler's wait counts conservative.
-template <int LAYOUT>
-__device__ __forceinline__ Pref load_block(const GemvArgs& a, const LaneBlock& b) {
+template <int LAYOUT, class SIDE>
+__device__ __forceinline__ Pref load_block(const GemvArgs& a, const LaneBlock& b, const SIDE& side) {
   Pref p = {0, 0, 0, 0, 0, 0, 0};
   if constexpr (LAYOUT == LEECH_PLANES14) {
     const u32x4 w = *(const u32x4*)record_window<kPlanes14Bytes>(a.main, b, p.sh);
@@ -212,9 +272,9 @@ __device__ __forceinline__ Pref load_block(const GemvArgs& a, const LaneBlock& b
     const u32x3 w = *(const u32x3*)record_window<kPlanes12Bytes>(a.main, b, p.sh);
     p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
   } else if constexpr (LAYOUT == LEECH_SLOT32) {
-    const uint8_t* ent = a.side0 + b.unit * kUnitEntryBytes;
-    const uint64_t bits = *(const uint64_t*)ent;
-    const uint32_t base = *(const uint32_t*)(ent + 8);
+    uint64_t bits;
+    uint32_t base;
+    side.unit_entry(a.side0, b.unit, bits, base);
     const uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << b.ul) - 1ull));
     const uint32_t* rec = (const uint32_t*)(a.main + (uint64_t)base * 4) +
                           (b.ul * (uint32_t)kSlot32Small + nbelow * (uint32_t)(kSlot32Large - kSlot32Small)) / 4;
@@ -247,18 +307,20 @@ __device__ __forceinline__ void planes14_fields(uint32_t w0, uint32_t w1, uint32
 // tab(e) returns the LdsEntry of e and g70(class) the G70Entry of a class
 // (from LDS in the GEMV, built from the global table in the verification
 // decode); cw(rank) is the Golay codeword of a rank.
-template <int LAYOUT, class TAB, class G70, class CW>
+template <int LAYOUT, class TAB, class G70, class CW, class SIDE>
 __device__ __forceinline__ void decode_block(const GemvArgs& a, const LaneBlock& b, const Pref& p,
-                                             TAB tab, G70 g70, CW cw, uint32_t h[12], uint32_t& e) {
+                                             TAB tab, G70 g70, CW cw, const SIDE& side,
+                                             uint32_t h[12], uint32_t& e) {
   uint32_t p0 = 0, p1 = 0, p2 = 0, sm = 0;
   if constexpr (LAYOUT == LEECH_PLANES14) {
     planes14_fields(p.w0, p.w1, p.w2, p.w3, p.sh, e, p0, p1, p2, sm);
   } else if constexpr (LAYOUT == LEECH_PLANES12X) {
     const uint32_t field = p.w2 >> kP12ExcShift;
     if (field) {      // five-level block: exact Planes14 record from the tile's list
-      const uint64_t ex = (uint64_t)(((const uint32_t*)a.side1)[b.tile] + field - 1);
-      const u32x4 w = *(const u32x4*)(a.side0 + ((ex * kPlanes14Bytes) & ~3ull));
-      planes14_fields(w.x, w.y, w.z, w.w, (uint32_t)(ex & 1) * 16u, e, p0, p1, p2, sm);
+      const uint64_t ex = (uint64_t)(side.p12_base(b.tile) + field - 1);
+      uint32_t w[4], sh;
+      side.exc_window(ex, w, sh);
+      planes14_fields(w[0], w[1], w[2], w[3], sh, e, p0, p1, p2, sm);
     } else {
       // two-plane level (0..3) -> code planes of level + 1, bit-parallel
       e = p.w0 & 1023u;
@@ -283,12 +345,13 @@ __device__ __forceinline__ void decode_block(const GemvArgs& a, const LaneBlock&
   } else if constexpr (LAYOUT == LEECH_GOLAY70) {
     const uint32_t r0 = align(p.w1, p.w0, p.sh), r1 = align(p.w2, p.w1, p.sh), r2 = p.w2 >> p.sh;
     if ((r2 >> 6) & 1u) {   // exception: exact Planes14 record located by the unit entry
-      const uint8_t* ent = a.side1 + b.unit * kUnitEntryBytes;
-      const uint64_t bits = *(const uint64_t*)ent;
-      const uint32_t base = *(const uint32_t*)(ent + 8);
+      uint64_t bits;
+      uint32_t base;
+      side.unit_entry(a.side1, b.unit, bits, base);
       const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << b.ul) - 1ull));
-      const u32x4 w = *(const u32x4*)(a.side0 + ((ex * kPlanes14Bytes) & ~3ull));
-      planes14_fields(w.x, w.y, w.z, w.w, (uint32_t)(ex & 1) * 16u, e, p0, p1, p2, sm);
+      uint32_t w[4], sh;
+      side.exc_window(ex, w, sh);
+      planes14_fields(w[0], w[1], w[2], w[3], sh, e, p0, p1, p2, sm);
     } else {
       e = r0 & 1023u;
       const uint32_t side = cw((r0 >> 10) & 0xFFFu);
@@ -372,7 +435,7 @@ __device__ __forceinline__ void store_x_block(const XBlock& xb, uint32_t* dst) {
 
 // ------------------------------------------------------------------- GEMV
 template <int LAYOUT>
-__global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
+__global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int64_t nb = a.nb;
   uint32_t* xs = (uint32_t*)smem;                                   // nb × 12 x pairs
@@ -382,7 +445,13 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
   G70Entry* gs = (G70Entry*)(smem + xbytes + tbytes);                // Golay70: 512 entries
   uint32_t* cws = (uint32_t*)(smem + xbytes + tbytes + 512 * sizeof(G70Entry));  // 4096 words
   const size_t gbytes = (LAYOUT == LEECH_GOLAY70) ? 512 * sizeof(G70Entry) + 4096 * 4 : 0;
-  float* red = (float*)(smem + xbytes + tbytes + gbytes);          // waves × 64
+  constexpr bool kUnits = LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
+  constexpr bool kExc = LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
+  uint8_t* units_lds = smem + xbytes + tbytes + gbytes;             // groups × 16 B
+  const size_t ubytes = kUnits ? (size_t)a.groups * kUnitEntryBytes : 0;
+  uint8_t* exc_lds = units_lds + ubytes;                              // ≤ kExcLdsBytes
+  const size_t ebytes = kExc ? kExcLdsBytes : 0;
+  float* red = (float*)(exc_lds + ebytes);                          // waves × 64
 
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int tile = (int)blockIdx.x;
@@ -415,10 +484,39 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
     return b;
   };
 
+  // Side data of the tile: its unit entries (Slot32, Golay70) and the range of
+  // its exception records (Planes12x, Golay70), copied to LDS below.
+  const GlobalSide gside{&a};
+  LdsSide side{&a, exc_lds, 0, false, units_lds, tile * groups, 0u};
+  uint64_t exc_chunks = 0;
+  if constexpr (kExc) {
+    uint64_t e0, e1;
+    if constexpr (LAYOUT == LEECH_PLANES12X) {
+      e0 = ((const uint32_t*)a.side1)[tile];
+      e1 = tile + 1 < a.tiles ? ((const uint32_t*)a.side1)[tile + 1] : a.n_exc;
+      side.p12base = (uint32_t)e0;
+    } else {
+      uint64_t bits;
+      uint32_t b0, b1 = 0;
+      gside.unit_entry(a.side1, tile * groups, bits, b0);
+      if (tile + 1 < a.tiles) gside.unit_entry(a.side1, (tile + 1) * groups, bits, b1);
+      e0 = b0;
+      e1 = tile + 1 < a.tiles ? b1 : a.n_exc;
+    }
+    side.exc_start = (e0 * kPlanes14Bytes) & ~15ull;
+    // the window of record e is 16 bytes from (14·e) & ~3, so the tile's
+    // windows end by 14·e1 + 2; rounded up to 16 this stays inside side0's
+    // 16 bytes of padding
+    const uint64_t end = e1 * kPlanes14Bytes + 2;
+    exc_chunks = (end - side.exc_start + 15) / 16;
+    side.exc_in_lds = exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
+  }
+
   // Prologue, ordered for the in-order load counter: first the L2-resident
-  // staging loads (x blocks, class table), then the units' record loads, then
-  // the LDS writes, which wait only for the older staging loads.
+  // staging loads (x blocks, class table, side data), then the units' record
+  // loads, then the LDS writes, which wait only for the older staging loads.
   constexpr int kXPer = 2, kTPer = 2;          // staged items per thread held in registers
+  constexpr int kEPer = kExcLdsBytes / 16 / 512, kUPer = 2;
   // rare overflow first (nb > kXPer·threads, or fewer threads than table
   // entries / kTPer): loads of unknown count here, before the ordered ones
   for (int64_t j = tid + (int64_t)kXPer * nthr; j < nb; j += nthr)
@@ -430,6 +528,14 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
     for (int c = tid; c < 512; c += nthr) gs[c] = make_g70(a.table, (uint32_t)c);
     for (int k = tid; k < 1024; k += nthr) ((u32x4a*)cws)[k] = ((const u32x4a*)a.codewords)[k];
   }
+  const uint8_t* side_units = LAYOUT == LEECH_SLOT32 ? a.side0 : a.side1;
+  if constexpr (kUnits)
+    for (int u = tid + kUPer * nthr; u < groups; u += nthr)
+      ((u32x4a*)units_lds)[u] = ((const u32x4a*)side_units)[tile * groups + u];
+  if constexpr (kExc)
+    if (side.exc_in_lds)
+      for (int64_t c = tid + (int64_t)kEPer * nthr; c < (int64_t)exc_chunks; c += nthr)
+        ((u32x4a*)exc_lds)[c] = ((const u32x4a*)(a.side0 + side.exc_start))[c];
   XBlock xr[kXPer];
 #pragma unroll
   for (int q = 0; q < kXPer; ++q) {
@@ -441,10 +547,24 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
 #pragma unroll
     for (int q = 0; q < kTPer; ++q) tr[q] = *(const u32x4a*)&a.table[(tid + q * nthr) & 511];
   }
+  u32x4a ur[kUPer], er[kEPer];
+  if constexpr (kUnits) {
+#pragma unroll
+    for (int q = 0; q < kUPer; ++q)
+      ur[q] = ((const u32x4a*)side_units)[tile * groups + min(tid + q * nthr, groups - 1)];
+  }
+  if constexpr (kExc) {
+    if (side.exc_in_lds) {
+#pragma unroll
+      for (int q = 0; q < kEPer; ++q)
+        er[q] = ((const u32x4a*)(a.side0 + side.exc_start))[min((int64_t)(tid + q * nthr),
+                                                                  (int64_t)exc_chunks - 1)];
+    }
+  }
   Pref pf[kPrefetch];
 #pragma unroll
   for (int d = 0; d < kPrefetch; ++d) {
-    pf[d] = load_block<LAYOUT>(a, unit_block(wave + d * waves));
+    pf[d] = load_block<LAYOUT>(a, unit_block(wave + d * waves), gside);
     __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
   }
 #pragma unroll
@@ -464,6 +584,18 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
         t.nlev = tr[q].w & 0xFFu;
         ts[e] = t;
       }
+    }
+  }
+  if constexpr (kUnits) {
+#pragma unroll
+    for (int q = 0; q < kUPer; ++q)
+      if (tid + q * nthr < groups) ((u32x4a*)units_lds)[tid + q * nthr] = ur[q];
+  }
+  if constexpr (kExc) {
+    if (side.exc_in_lds) {
+#pragma unroll
+      for (int q = 0; q < kEPer; ++q)
+        if (tid + q * nthr < (int64_t)exc_chunks) ((u32x4a*)exc_lds)[tid + q * nthr] = er[q];
     }
   }
   __syncthreads();
@@ -488,7 +620,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
       acc += b.valid ? s : 0.0f;
     } else {
       uint32_t h[12], e;
-      decode_block<LAYOUT>(a, b, p, tab, g70, cw, h, e);
+      decode_block<LAYOUT>(a, b, p, tab, g70, cw, side, h, e);
       float s = 0.0f;
 #pragma unroll
       for (int k = 0; k < 12; ++k) s = __builtin_amdgcn_fdot2(as_h2(h[k]), as_h2(xw[k]), s, false);
@@ -509,7 +641,7 @@ __global__ __launch_bounds__(1024) void gemv_kernel(GemvArgs a) {
     for (int d = 0; d < kPrefetch; ++d) {
       const int g = wave + (done + d) * waves;
       process(pf[d], g);
-      pf[d] = load_block<LAYOUT>(a, unit_block(g + kPrefetch * waves));
+      pf[d] = load_block<LAYOUT>(a, unit_block(g + kPrefetch * waves), side);
     }
   }
   // the last ≤ kPrefetch units are in flight: straight-line, no refills
@@ -540,12 +672,13 @@ __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, u
   const int R_t = (int)min((int64_t)a.R, a.M - tile * a.R);
   LaneBlock b = lane_block(a, tile, R_t, g, (int)(r % a.R), (int)(j % a.C));
   b.loff = b.ul * Stride<LAYOUT>::v;
-  const Pref p = load_block<LAYOUT>(a, b);
+  const GlobalSide side{&a};
+  const Pref p = load_block<LAYOUT>(a, b, side);
   auto tab = [&](uint32_t e) -> LdsEntry { return make_entry(a.table, e, 1.0f, 1.0f); };
   auto g70 = [&](uint32_t c) -> G70Entry { return make_g70(a.table, c); };
   auto cw = [&](uint32_t rk) -> uint32_t { return a.codewords[rk]; };
   uint32_t h[12], e;
-  decode_block<LAYOUT>(a, b, p, tab, g70, cw, h, e);
+  decode_block<LAYOUT>(a, b, p, tab, g70, cw, side, h, e);
   int8_t z[kDim];
 #pragma unroll
   for (int k = 0; k < 12; ++k) {
@@ -607,7 +740,7 @@ static int waves_for(int64_t groups) {
   static const int cap = [] {
     const char* v = std::getenv("LEECH_WAVES");
     const int w = v ? std::atoi(v) : 0;
-    return (w >= 1 && w <= 16) ? w : 8;
+    return (w >= 1 && w <= kMaxWaves) ? w : kMaxWaves;
   }();
   return (int)std::max<int64_t>(1, std::min<int64_t>(cap, groups));
 }
@@ -630,13 +763,18 @@ static GemvArgs make_args(const leech_layout_desc* d) {
   a.R = kWave / d->lane_cols;
   a.groups = (d->nb + a.C - 1) / a.C;
   a.waves = waves_for(a.groups);
+  a.tiles = (d->M + a.R - 1) / a.R;
+  a.n_exc = d->n_exceptions;
   return a;
 }
 
 template <int LAYOUT>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
+  const bool units = LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
+  const bool exc = LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
   return (size_t)a.nb * 48 + (LAYOUT == kNoWeights ? 0 : 1024 * sizeof(LdsEntry)) +
          (LAYOUT == LEECH_GOLAY70 ? 512 * sizeof(G70Entry) + 4096 * 4 : 0) +
+         (units ? (size_t)a.groups * kUnitEntryBytes : 0) + (exc ? kExcLdsBytes : 0) +
          (size_t)a.waves * 64 * 4;
 }
 
