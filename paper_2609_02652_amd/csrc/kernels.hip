@@ -18,6 +18,16 @@
 // the waves through LDS, in a fixed order, so y depends only on
 // (M, Kpad, lane_cols), never on the layout.
 //
+// Addressing.  Records and scales are read with raw buffer loads: the
+// workgroup's buffer descriptor starts at its tile, the unit's offset is a
+// scalar, and the lane's offset inside the unit is a per-lane constant, so a
+// step spends no vector instructions on addresses.  Every unit of a tile but
+// the last (narrower) column group is full width, so the pipelined loop uses
+// one set of lane constants and needs no per-lane masking: lanes of rows past
+// the matrix decode a stand-in and their sums are never written.  The last
+// column group is loaded in the prologue and added by one wave at the end,
+// with lanes past the last column reading zero x.
+//
 // Decode.  The paper's per-coordinate predicated tree is replaced, since the
 // MI355X has about an order of magnitude less VALU issue per HBM byte than the
 // paper's GPU: the four 24-bit planes of a block (p0, p1, p2 and the inverted
@@ -45,8 +55,25 @@ typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
 typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));
 
 constexpr int kNoWeights = 99;   // layout id of the no-weights control
-constexpr int kPrefetch = 8;     // units in flight per wavefront
+#ifndef LEECH_PREFETCH
+#define LEECH_PREFETCH 8
+#endif
+constexpr int kPrefetch = LEECH_PREFETCH;     // units in flight per wavefront
 constexpr float kTwo24 = 16777216.0f;
+// Waves per GEMV workgroup, at most: 8 waves leave each lane up to 256 VGPRs,
+// so the eight prefetch slots and the exception-path decode stay in registers.
+constexpr int kMaxWaves = 8;
+constexpr int kExcLdsBytes = 32 * 1024;   // a tile's exception records staged in LDS
+constexpr int kTableBytes = 1024 * 16;    // LDS class-table entries (class | gain << 9)
+// Raw buffer descriptor, word 3, for the gfx9 family (32-bit elements, no
+// swizzle); loads carry the non-temporal hint: records and scales are read once.
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kStreamed = 2;
+
+template <int LAYOUT> struct Stride { static constexpr uint32_t v = 0; };
+template <> struct Stride<LEECH_PLANES14> { static constexpr uint32_t v = kPlanes14Bytes; };
+template <> struct Stride<LEECH_PLANES12X> { static constexpr uint32_t v = kPlanes12Bytes; };
+template <> struct Stride<LEECH_GOLAY70> { static constexpr uint32_t v = kGolay70Bytes; };
 
 struct GemvArgs {
   const uint8_t* main;
@@ -62,15 +89,11 @@ struct GemvArgs {
   int C, R, waves;
   int64_t tiles;
   uint64_t n_exc;               // exception records (Planes12x, Golay70)
+  uint64_t main_bytes;
 };
 
-// Waves per GEMV workgroup, at most: 8 waves leave each lane up to 256 VGPRs,
-// so the eight prefetch slots and the exception-path decode stay in registers.
-constexpr int kMaxWaves = 8;
-constexpr int kExcLdsBytes = 32 * 1024;   // a tile's exception records staged in LDS
-
 // Where side data comes from: global memory (verification decode, and the
-// GEMV's first prefetches) or the workgroup's LDS copies (the GEMV's loop).
+// GEMV prologue before LDS is written), or the tile's copy in LDS.
 struct GlobalSide {
   const GemvArgs* a;
   __device__ __forceinline__ uint32_t p12_base(int tile) const {
@@ -122,12 +145,13 @@ __device__ __forceinline__ void LdsSide::exc_window(uint64_t ex, uint32_t w[4], 
   sh = (uint32_t)(goff & 2) * 8u;
 }
 
-// Per-(class, gain) entry staged in LDS; e = class | gain << 9.
+// Per-(class, gain) entry staged in LDS at byte (class | gain << 9) · 16.
 struct LdsEntry {
   uint32_t tlo, thi;    // v_perm table (DevClass::perm)
   float factor;         // 2^24 · centroid[gain] / (4√m)
   uint32_t nlev;        // level count
 };
+static_assert(sizeof(LdsEntry) * 1024 == kTableBytes, "table entries are 16 bytes");
 // Golay70 per-class entry staged in LDS (index = class id).
 struct G70Entry {
   uint32_t alo, ahi;    // |value| at side·4 + code
@@ -140,16 +164,20 @@ __device__ __forceinline__ uint32_t align(uint32_t hi, uint32_t lo, uint32_t s) 
 __device__ __forceinline__ uint32_t perm(uint32_t s0, uint32_t s1, uint32_t sel) {
   return __builtin_amdgcn_perm(s0, s1, sel);
 }
+// (m & a) | (~m & b) as one v_bfi_b32: left to itself the compiler splits the
+// nibble transpose's bit-field inserts into and / and_or pairs.
 __device__ __forceinline__ uint32_t bfi(uint32_t m, uint32_t a, uint32_t b) {
-  return (m & a) | (~m & b);
+  uint32_t r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "s"(m), "v"(a), "v"(b));
+  return r;
 }
 // Reinterpret a 32-bit word as two binary16 values.  Takes the word by value:
 // applying __builtin_bit_cast directly to an ext_vector element (w.y) reads
 // element 0 with this compiler, so vector elements go through this function.
 __device__ __forceinline__ half2_t as_h2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
 
-__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+__device__ __forceinline__ _Float16 as_half(uint32_t h) {
+  return __builtin_bit_cast(_Float16, (uint16_t)h);
 }
 
 // 4×4 bit transpose inside every nibble: on return n[r] bit (4g + q) is bit
@@ -177,16 +205,17 @@ __device__ __forceinline__ void pair_sources(uint32_t N, uint32_t s[3]) {
   s[2] = perm(R, N, 0x05050101u);
 }
 
-// Planes core: nibble (c0, c1, c2, ¬s) per coordinate, with c = level + 1 the
-// level code -> 12 binary16 pairs.  Selector byte for the low half: the code
-// (table bytes 1..5 hold |z| of levels 0..4); for the high half: 0 (table
-// byte 0 = 0x80) when negative, 8 when not (v_perm's selector 8 replicates
-// bit 7 of table byte 1, a magnitude below 0x80, giving 0x00).  Pair 3r + k
-// of h[] covers the coordinates listed by pair_sources.
-__device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t sm,
+// Planes core: nibble (c0, c1, c2, pos) per coordinate, with c = level + 1 the
+// level code and pos = 1 for a non-negative coordinate -> 12 binary16 pairs.
+// Selector byte for the low half: the code (table bytes 1..5 hold |z| of
+// levels 0..4); for the high half: 0 (table byte 0 = 0x80) when negative, 8
+// when not (v_perm's selector 8 replicates bit 7 of table byte 1, a magnitude
+// below 0x80, giving 0x00).  Pair 3r + k of h[] covers the coordinates listed
+// by pair_sources.
+__device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t pos,
                                             uint32_t tlo, uint32_t thi, uint32_t h[12]) {
   uint32_t n[4];
-  nibble_transpose(p0, p1, p2, ~sm, n);
+  nibble_transpose(p0, p1, p2, pos, n);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     uint32_t s[3];
@@ -222,109 +251,69 @@ __device__ __forceinline__ void pair_coords(int k, int& c0, int& c1) {
 }
 
 // ---------------------------------------------------------- per-block reads
-// Where a lane's block sits: storage index ubase + ul, with ubase the first
-// block of the unit (uniform across the wavefront) and ul the lane's position
-// inside the unit.
-struct LaneBlock {
-  int64_t ubase;     // storage index of the unit's first block (wave-uniform)
-  int32_t unit;      // tile·groups + g (wave-uniform)
-  int32_t tile;      // (wave-uniform)
-  uint32_t ul;       // position inside the unit
-  uint32_t loff;     // ul · record stride (fixed-stride layouts)
-  bool valid;
-  __device__ __forceinline__ uint64_t idx() const { return (uint64_t)ubase + ul; }
+// A lane's place in a unit: its position ul (0 for a lane without a block,
+// which then reads block 0 as a stand-in) and, for the fixed-stride layouts,
+// the record window: a 4-aligned byte offset from the unit's base and the
+// record's bit offset sh inside it.  esh is the funnel-shift amount that brings
+// a Planes14 record's class|gain field to bits 4..13 of word 3 (entry · 16).
+struct Lane {
+  uint32_t ul;
+  uint32_t rec;
+  uint32_t sh;
+  uint32_t esh;
 };
-
-template <int LAYOUT> struct Stride { static constexpr uint32_t v = 0; };
-template <> struct Stride<LEECH_PLANES14> { static constexpr uint32_t v = kPlanes14Bytes; };
-template <> struct Stride<LEECH_PLANES12X> { static constexpr uint32_t v = kPlanes12Bytes; };
-template <> struct Stride<LEECH_GOLAY70> { static constexpr uint32_t v = kGolay70Bytes; };
+// u: the unit base's byte offset modulo 4
+__device__ __forceinline__ Lane lane_place(uint32_t ul, uint32_t stride, uint32_t u) {
+  const uint32_t off = ul * stride + u;
+  const uint32_t sh = (off & 3u) * 8u;
+  return Lane{ul, off & ~3u, sh, (sh + 28u) & 31u};
+}
 
 // Words a lane prefetches for one block.
 struct Pref {
   uint32_t w0, w1, w2, w3, w4;
   uint32_t scale;
-  uint32_t sh;       // bit offset of the record inside its first word
+  uint32_t sh, esh;
 };
 
-// Window of n words holding the record of block i at stride `stride` bytes:
-// the wave-uniform part of the byte offset goes into the base pointer, the
-// lane part stays a 32-bit offset.
-template <int STRIDE>
-__device__ __forceinline__ const uint32_t* record_window(const uint8_t* base, const LaneBlock& b,
-                                                         uint32_t& sh) {
-  const uint64_t U = (uint64_t)b.ubase * STRIDE;
-  const uint32_t lo = (uint32_t)(U & 3u) + b.loff;
-  sh = (lo & 3u) * 8u;
-  return (const uint32_t*)(base + (U & ~3ull) + (lo & ~3u));
-}
-
-// Loads are issued unconditionally (callers hand in a clamped, in-bounds
-// block for lanes or units that do not exist and ignore the data): branches
-// around loads would make the compiler's wait counts conservative.
-template <int LAYOUT, class SIDE>
-__device__ __forceinline__ Pref load_block(const GemvArgs& a, const LaneBlock& b, const SIDE& side) {
-  Pref p = {0, 0, 0, 0, 0, 0, 0};
-  if constexpr (LAYOUT == LEECH_PLANES14) {
-    const u32x4 w = *(const u32x4*)record_window<kPlanes14Bytes>(a.main, b, p.sh);
-    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w;
-  } else if constexpr (LAYOUT == LEECH_PLANES12X) {
-    const u32x3 w = *(const u32x3*)record_window<kPlanes12Bytes>(a.main, b, p.sh);
-    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
-  } else if constexpr (LAYOUT == LEECH_SLOT32) {
-    uint64_t bits;
-    uint32_t base;
-    side.unit_entry(a.side0, b.unit, bits, base);
-    const uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << b.ul) - 1ull));
-    const uint32_t* rec = (const uint32_t*)(a.main + (uint64_t)base * 4) +
-                          (b.ul * (uint32_t)kSlot32Small + nbelow * (uint32_t)(kSlot32Large - kSlot32Small)) / 4;
-    const u32x4 w = *(const u32x4*)rec;
-    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w; p.w4 = rec[4];
-  } else if constexpr (LAYOUT == LEECH_GOLAY70) {
-    const u32x3 w = *(const u32x3*)record_window<kGolay70Bytes>(a.main, b, p.sh);
-    p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
-  }
-  if constexpr (LAYOUT != kNoWeights)
-    p.scale = *(const uint16_t*)((const uint8_t*)(a.scale + b.ubase) + (uint32_t)(b.ul * 2u));
-  return p;
-}
-
-// Planes14 fields of the four-word window starting at byte (14·i) & ~3: the
-// record begins 0 or 16 bits in (§2.3: a four-word window, shift 0 or 16).
+// Planes14 fields of the four-word window whose record starts at bit sh (0 or
+// 16): every plane starts on a 32-bit boundary of the record, so one funnel
+// shift each gives p0, p1, p2 in bits 0..23 with one byte of the inverted sign
+// mask above; two byte permutes gather that mask.  e16 = (class | gain << 9)·16,
+// the entry's LDS byte address.
 __device__ __forceinline__ void planes14_fields(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
-                                                uint32_t sh, uint32_t& e, uint32_t& p0,
-                                                uint32_t& p1, uint32_t& p2, uint32_t& sm) {
-  const uint32_t r0 = align(w1, w0, sh), r1 = align(w2, w1, sh), r2 = align(w3, w2, sh);
-  const uint32_t r3 = w3 >> sh;
-  e = r0 & 1023u;              // class | gain << 9
-  sm = align(r1, r0, 10);      // plane bits above 23 are never read
-  p0 = r1 >> 2;
-  p1 = align(r2, r1, 26);
-  p2 = align(r3, r2, 18);
+                                                uint32_t sh, uint32_t esh, uint32_t& e16,
+                                                uint32_t& p0, uint32_t& p1, uint32_t& p2,
+                                                uint32_t& pos) {
+  p0 = align(w1, w0, sh);
+  p1 = align(w2, w1, sh);
+  p2 = align(w3, w2, sh);
+  pos = perm(p2, perm(p1, p0, 0x0C0C0703u), 0x0C070100u);
+  e16 = align(w3, w3, esh) & 0x3FF0u;
 }
 
-// Decode one block into 12 binary16 pairs and its table entry index.
-// tab(e) returns the LdsEntry of e and g70(class) the G70Entry of a class
+// Decode one block into 12 binary16 pairs and its table entry's byte address.
+// tab(e16) returns the LdsEntry at e16 and g70(class) the G70Entry of a class
 // (from LDS in the GEMV, built from the global table in the verification
 // decode); cw(rank) is the Golay codeword of a rank.
 template <int LAYOUT, class TAB, class G70, class CW, class SIDE>
-__device__ __forceinline__ void decode_block(const GemvArgs& a, const LaneBlock& b, const Pref& p,
+__device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int tile, int unit,
                                              TAB tab, G70 g70, CW cw, const SIDE& side,
-                                             uint32_t h[12], uint32_t& e) {
-  uint32_t p0 = 0, p1 = 0, p2 = 0, sm = 0;
+                                             const GemvArgs& a, uint32_t h[12], uint32_t& e16) {
+  uint32_t p0 = 0, p1 = 0, p2 = 0, pos = 0;
   if constexpr (LAYOUT == LEECH_PLANES14) {
-    planes14_fields(p.w0, p.w1, p.w2, p.w3, p.sh, e, p0, p1, p2, sm);
+    planes14_fields(p.w0, p.w1, p.w2, p.w3, p.sh, p.esh, e16, p0, p1, p2, pos);
   } else if constexpr (LAYOUT == LEECH_PLANES12X) {
     const uint32_t field = p.w2 >> kP12ExcShift;
     if (field) {      // five-level block: exact Planes14 record from the tile's list
-      const uint64_t ex = (uint64_t)(side.p12_base(b.tile) + field - 1);
+      const uint64_t ex = (uint64_t)(side.p12_base(tile) + field - 1);
       uint32_t w[4], sh;
       side.exc_window(ex, w, sh);
-      planes14_fields(w[0], w[1], w[2], w[3], sh, e, p0, p1, p2, sm);
+      planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
     } else {
       // two-plane level (0..3) -> code planes of level + 1, bit-parallel
-      e = p.w0 & 1023u;
-      sm = align(p.w1, p.w0, 10);
+      e16 = (p.w0 << 4) & 0x3FF0u;
+      pos = ~align(p.w1, p.w0, 10);
       const uint32_t l0 = p.w1 >> 2, l1 = align(p.w2, p.w1, 26);
       p0 = ~l0;
       p1 = l0 ^ l1;
@@ -332,9 +321,9 @@ __device__ __forceinline__ void decode_block(const GemvArgs& a, const LaneBlock&
     }
   } else if constexpr (LAYOUT == LEECH_SLOT32) {
     // one-hot masks of levels 1..4 -> code planes of level + 1 (codes 1..5)
-    e = p.w0 & 1023u;
-    const uint32_t L = tab(e).nlev;
-    sm = align(p.w1, p.w0, 10);
+    e16 = (p.w0 << 4) & 0x3FF0u;
+    const uint32_t L = tab(e16).nlev;
+    pos = ~align(p.w1, p.w0, 10);
     const uint32_t m1 = L > 1 ? p.w1 >> 2 : 0u;
     const uint32_t m2 = L > 2 ? align(p.w2, p.w1, 26) : 0u;
     const uint32_t m3 = L > 3 ? align(p.w3, p.w2, 18) : 0u;
@@ -347,33 +336,76 @@ __device__ __forceinline__ void decode_block(const GemvArgs& a, const LaneBlock&
     if ((r2 >> 6) & 1u) {   // exception: exact Planes14 record located by the unit entry
       uint64_t bits;
       uint32_t base;
-      side.unit_entry(a.side1, b.unit, bits, base);
-      const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << b.ul) - 1ull));
+      side.unit_entry(a.side1, unit, bits, base);
+      const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << ul) - 1ull));
       uint32_t w[4], sh;
       side.exc_window(ex, w, sh);
-      planes14_fields(w[0], w[1], w[2], w[3], sh, e, p0, p1, p2, sm);
+      planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
     } else {
-      e = r0 & 1023u;
-      const uint32_t side = cw((r0 >> 10) & 0xFFFu);
-      golay70_core(align(r1, r0, 22), align(r2, r1, 14), side, g70(e & 511u), h);
+      e16 = (r0 << 4) & 0x3FF0u;
+      const uint32_t side_bits = cw((r0 >> 10) & 0xFFFu);
+      golay70_core(align(r1, r0, 22), align(r2, r1, 14), side_bits, g70((e16 >> 4) & 511u), h);
       return;
     }
   }
-  const LdsEntry t = tab(e);
-  planes_core(p0, p1, p2, sm, t.tlo, t.thi, h);
+  const LdsEntry t = tab(e16);
+  planes_core(p0, p1, p2, pos, t.tlo, t.thi, h);
 }
 
-__device__ __forceinline__ LaneBlock lane_block(const GemvArgs& a, int64_t tile, int R_t, int64_t g,
-                                                int rl, int cl) {
-  LaneBlock b;
-  const int C_g = (int)min((int64_t)a.C, a.nb - g * a.C);
-  b.valid = rl < R_t && cl < C_g;
-  b.ul = (uint32_t)(rl * C_g + cl);
-  b.loff = b.ul * Stride<LEECH_PLANES14>::v;   // overwritten per layout by the caller
-  b.tile = (int32_t)tile;
-  b.unit = (int32_t)(tile * a.groups + g);
-  b.ubase = tile * a.R * a.nb + g * R_t * a.C;
-  return b;
+// Per-workgroup view of the streams: buffer descriptors based at the tile's
+// first record and first scale, and the tile's shape.
+struct TileCtx {
+  __amdgpu_buffer_rsrc_t rec, sc;
+  int tile, R_t, C, groups;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t bytes) {
+  const uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)n, kRsrcWord3);
+}
+
+// Loads of unit g for a lane at place L.  EVEN: every unit base of the layout
+// is 4-aligned, so L is used as is; otherwise the lane's window is recomputed
+// from the unit base's offset modulo 4.  Loads are issued unconditionally
+// (callers hand in an in-bounds stand-in unit and ignore its data): branches
+// around loads would make the compiler's wait counts conservative.
+template <int LAYOUT, bool EVEN, class SIDE>
+__device__ __forceinline__ Pref load_unit(const GemvArgs& a, const TileCtx& t, const Lane& L, int g,
+                                          const SIDE& side) {
+  Pref p = {0, 0, 0, 0, 0, 0, 0, 0};
+  if constexpr (LAYOUT == kNoWeights) {
+    return p;
+  } else {
+    const uint32_t blk = (uint32_t)g * (uint32_t)(t.R_t * t.C);   // blocks before the unit
+    if constexpr (LAYOUT == LEECH_SLOT32) {
+      uint64_t bits;
+      uint32_t base;
+      side.unit_entry(a.side0, t.tile * t.groups + g, bits, base);
+      const uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << L.ul) - 1ull));
+      const uint32_t* rec = (const uint32_t*)(a.main + (uint64_t)base * 4) +
+                            (L.ul * (uint32_t)kSlot32Small +
+                             nbelow * (uint32_t)(kSlot32Large - kSlot32Small)) / 4;
+      const u32x4 w = *(const u32x4*)rec;
+      p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w; p.w4 = rec[4];
+    } else {
+      constexpr uint32_t S = Stride<LAYOUT>::v;
+      const uint32_t ub = blk * S;
+      Lane l = L;
+      if constexpr (!EVEN) l = lane_place(L.ul, S, ub & 3u);
+      const int soff = (int)(ub & ~3u);
+      if constexpr (LAYOUT == LEECH_PLANES14) {
+        const u32x4a w = __builtin_amdgcn_raw_buffer_load_b128(t.rec, (int)l.rec, soff, kStreamed);
+        p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w;
+      } else {
+        const u32x3 w = __builtin_amdgcn_raw_buffer_load_b96(t.rec, (int)l.rec, soff, kStreamed);
+        p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
+      }
+      p.sh = l.sh;
+      p.esh = l.esh;
+    }
+    p.scale = __builtin_amdgcn_raw_buffer_load_b16(t.sc, (int)(L.ul * 2u), (int)(blk * 2u), kStreamed);
+    return p;
+  }
 }
 
 // The LDS entries, built from the device table: one 16-byte load per entry.
@@ -383,7 +415,7 @@ __device__ __forceinline__ LdsEntry make_entry(const DevClass* tab, uint32_t e, 
   LdsEntry t;
   t.tlo = d.x;
   t.thi = d.y;
-  t.factor = __builtin_bit_cast(float, (uint32_t)d.z) * ((e >> 9) ? cen1 : cen0) * kTwo24;
+  t.factor = __builtin_bit_cast(float, (uint32_t)d.z) * kTwo24 * ((e >> 9) ? cen1 : cen0);
   t.nlev = d.w & 0xFFu;
   return t;
 }
@@ -433,56 +465,77 @@ __device__ __forceinline__ void store_x_block(const XBlock& xb, uint32_t* dst) {
   d[2] = u32x4a{o[8], o[9], o[10], o[11]};
 }
 
+// s = Σ_k h[k]·x[k] over the 12 binary16 pairs, f32 accumulation; the first
+// product is a v_dot2_f32_f16 with a zero addend, where the compiler would
+// otherwise zero a register for the accumulate-in-place form.
+__device__ __forceinline__ float dot12(const uint32_t h[12], const uint32_t xw[12]) {
+  float s;
+  asm("v_dot2_f32_f16 %0, %1, %2, 0" : "=v"(s) : "v"(h[0]), "v"(xw[0]));
+#pragma unroll
+  for (int k = 1; k < 12; ++k) s = __builtin_amdgcn_fdot2(as_h2(h[k]), as_h2(xw[k]), s, false);
+  return s;
+}
+
 // ------------------------------------------------------------------- GEMV
+// LDS: the class table in a static array (entry e at byte e·16 of it, so a
+// decoded field is its own address), then, dynamically sized, x for groups·C
+// block columns (zero past nb), the Golay70 tables, the tile's side data, the
+// cross-wave reduction.
 template <int LAYOUT>
+__host__ __device__ constexpr bool has_units() {
+  return LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
+}
+template <int LAYOUT>
+__host__ __device__ constexpr bool has_exc() {
+  return LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
+}
+
+template <int LAYOUT, bool EVEN>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  __shared__ __attribute__((aligned(16))) LdsEntry ts[1024];
+  constexpr bool kW = LAYOUT != kNoWeights;
+  constexpr bool kUnits = has_units<LAYOUT>();
+  constexpr bool kExc = has_exc<LAYOUT>();
   const int64_t nb = a.nb;
-  uint32_t* xs = (uint32_t*)smem;                                   // nb × 12 x pairs
-  const size_t xbytes = (size_t)nb * 48;
-  LdsEntry* ts = (LdsEntry*)(smem + xbytes);                         // 1024 entries
-  const size_t tbytes = (LAYOUT == kNoWeights) ? 0 : 1024 * sizeof(LdsEntry);
-  G70Entry* gs = (G70Entry*)(smem + xbytes + tbytes);                // Golay70: 512 entries
-  uint32_t* cws = (uint32_t*)(smem + xbytes + tbytes + 512 * sizeof(G70Entry));  // 4096 words
-  const size_t gbytes = (LAYOUT == LEECH_GOLAY70) ? 512 * sizeof(G70Entry) + 4096 * 4 : 0;
-  constexpr bool kUnits = LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
-  constexpr bool kExc = LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
-  uint8_t* units_lds = smem + xbytes + tbytes + gbytes;             // groups × 16 B
-  const size_t ubytes = kUnits ? (size_t)a.groups * kUnitEntryBytes : 0;
-  uint8_t* exc_lds = units_lds + ubytes;                              // ≤ kExcLdsBytes
-  const size_t ebytes = kExc ? kExcLdsBytes : 0;
-  float* red = (float*)(exc_lds + ebytes);                          // waves × 64
+  const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
+  const int xblocks = groups * C;
+  uint32_t* xs = (uint32_t*)smem;                                       // xblocks × 12 x pairs
+  uint8_t* p = smem + (size_t)xblocks * 48;
+  G70Entry* gs = (G70Entry*)p;                                          // Golay70: 512 entries
+  uint32_t* cws = (uint32_t*)(p + 512 * sizeof(G70Entry));              // 4096 words
+  if constexpr (LAYOUT == LEECH_GOLAY70) p += 512 * sizeof(G70Entry) + 4096 * 4;
+  uint8_t* units_lds = p;                                               // groups × 16 B
+  if constexpr (kUnits) p += (size_t)groups * kUnitEntryBytes;
+  uint8_t* exc_lds = p;                                                 // ≤ kExcLdsBytes
+  if constexpr (kExc) p += kExcLdsBytes;
+  float* red = (float*)p;                                               // waves × 64
 
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int tile = (int)blockIdx.x;
   const int R_t = (int)min((int64_t)a.R, a.M - (int64_t)tile * a.R);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
-  const int rl = lane / a.C, cl = lane % a.C;
-  const int groups = (int)a.groups, waves = a.waves;     // unit counts fit 32 bits
-  // lane constants: position inside a full unit and inside the narrower last
-  // one; a lane with no block there takes block 0 (in bounds) and is masked
-  const int C_last = (int)(a.nb - (int64_t)(groups - 1) * a.C);
+  const int rl = lane / C, cl = lane % C;
+  const int gf = groups - 1;                      // full-width column groups
+  const int C_last = (int)(nb - (int64_t)gf * C);
   const bool row_ok = rl < R_t, last_ok = row_ok && cl < C_last;
-  const uint32_t ul_f = row_ok ? (uint32_t)(rl * a.C + cl) : 0u;
-  const uint32_t ul_l = last_ok ? (uint32_t)(rl * C_last + cl) : 0u;
-  const uint32_t lo_f = ul_f * Stride<LAYOUT>::v, lo_l = ul_l * Stride<LAYOUT>::v;
-  const int64_t tile_base = (int64_t)tile * a.R * a.nb;
-  // the block of this lane in unit g (g wave-uniform); past the last unit an
-  // in-bounds stand-in with valid = false
-  auto unit_block = [&](int g) -> LaneBlock {
-    LaneBlock b;
-    const bool beyond = g >= groups;
-    g = beyond ? groups - 1 : g;
-    const bool last = g == groups - 1;
-    b.valid = !beyond && (last ? last_ok : row_ok);
-    b.ul = last ? ul_l : ul_f;
-    b.loff = last ? lo_l : lo_f;
-    b.tile = tile;
-    b.unit = tile * groups + g;
-    b.ubase = tile_base + (int64_t)g * (R_t * a.C);
-    return b;
-  };
+  constexpr uint32_t S = Stride<LAYOUT>::v;
+  const Lane Lf = lane_place(row_ok ? (uint32_t)(rl * C + cl) : 0u, S, 0u);
+  const Lane Ll = lane_place(last_ok ? (uint32_t)(rl * C_last + cl) : 0u, S, 0u);
+  // the pipeline's lane place and its stand-in unit: a full unit when there is
+  // one, else the last (then the pipeline processes nothing)
+  const Lane Lp = gf > 0 ? Lf : Ll;
+  const int g_stand = gf > 0 ? gf - 1 : gf;
+  const uint64_t tile_blk = (uint64_t)tile * a.R * (uint64_t)nb;
+  const uint64_t tile_rec = tile_blk * S;
+  TileCtx t;
+  t.rec = make_rsrc(a.main + tile_rec, a.main_bytes - tile_rec);
+  t.sc = make_rsrc(a.scale + tile_blk, ((uint64_t)a.M * (uint64_t)nb - tile_blk) * 2);
+  t.tile = tile;
+  t.R_t = R_t;
+  t.C = C;
+  t.groups = groups;
 
   // Side data of the tile: its unit entries (Slot32, Golay70) and the range of
   // its exception records (Planes12x, Golay70), copied to LDS below.
@@ -512,18 +565,29 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     side.exc_in_lds = exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
   }
 
-  // Prologue, ordered for the in-order load counter: first the L2-resident
-  // staging loads (x blocks, class table, side data), then the units' record
-  // loads, then the LDS writes, which wait only for the older staging loads.
-  constexpr int kXPer = 2, kTPer = 2;          // staged items per thread held in registers
-  constexpr int kEPer = kExcLdsBytes / 16 / 512, kUPer = 2;
-  // rare overflow first (nb > kXPer·threads, or fewer threads than table
-  // entries / kTPer): loads of unknown count here, before the ordered ones
-  for (int64_t j = tid + (int64_t)kXPer * nthr; j < nb; j += nthr)
-    store_x_block(load_x_block(a.x + 24 * j), xs + 12 * j);
-  if constexpr (LAYOUT != kNoWeights)
-    for (int e = tid + kTPer * nthr; e < 1024; e += nthr)
-      ts[e] = make_entry(a.table, (uint32_t)e, a.cen0, a.cen1);
+  // Prologue, ordered for the in-order load counter: first the staging loads
+  // (x blocks, class table, side data), then the last column group's loads,
+  // then the pipeline's record loads, then the LDS writes, which wait only for
+  // the older staging loads.
+  constexpr int kXPer = 2;                     // x blocks per thread held in registers
+  constexpr int kEPer = kExcLdsBytes / 16 / (kMaxWaves * 64), kUPer = 2;
+  // rare overflow first (xblocks > kXPer·threads, or fewer threads than
+  // classes): loads of unknown count here, before the ordered ones.  Only the
+  // ball's class ids occur in a layout, so only their entries are staged, both
+  // gain entries of a class from one read of its table record.
+  for (int j = tid + kXPer * nthr; j < xblocks; j += nthr) {
+    if (j < nb) {
+      store_x_block(load_x_block(a.x + 24 * (int64_t)j), xs + 12 * j);
+    } else {
+      u32x4a* d = (u32x4a*)(xs + 12 * j);
+      d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
+    }
+  }
+  if constexpr (kW)
+    for (int c = tid + nthr; c < kBallClasses; c += nthr) {
+      ts[c] = make_entry(a.table, (uint32_t)c, a.cen0, a.cen1);
+      ts[c + 512] = make_entry(a.table, (uint32_t)c | 512u, a.cen0, a.cen1);
+    }
   if constexpr (LAYOUT == LEECH_GOLAY70) {
     for (int c = tid; c < 512; c += nthr) gs[c] = make_g70(a.table, (uint32_t)c);
     for (int k = tid; k < 1024; k += nthr) ((u32x4a*)cws)[k] = ((const u32x4a*)a.codewords)[k];
@@ -542,11 +606,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     const int64_t j = min(tid + (int64_t)q * nthr, nb - 1);    // clamped: loads stay unconditional
     xr[q] = load_x_block(a.x + 24 * j);
   }
-  u32x4a tr[kTPer];
-  if constexpr (LAYOUT != kNoWeights) {
-#pragma unroll
-    for (int q = 0; q < kTPer; ++q) tr[q] = *(const u32x4a*)&a.table[(tid + q * nthr) & 511];
-  }
+  u32x4a tr = {0, 0, 0, 0};
+  if constexpr (kW) tr = *(const u32x4a*)&a.table[min(tid, kBallClasses - 1)];
   u32x4a ur[kUPer], er[kEPer];
   if constexpr (kUnits) {
 #pragma unroll
@@ -561,29 +622,34 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
                                                                   (int64_t)exc_chunks - 1)];
     }
   }
+  const Pref plast = load_unit<LAYOUT, EVEN>(a, t, Ll, gf, gside);
   Pref pf[kPrefetch];
 #pragma unroll
   for (int d = 0; d < kPrefetch; ++d) {
-    pf[d] = load_block<LAYOUT>(a, unit_block(wave + d * waves), gside);
+    pf[d] = load_unit<LAYOUT, EVEN>(a, t, Lp, min(wave + d * waves, g_stand), gside);
     __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
   }
 #pragma unroll
   for (int q = 0; q < kXPer; ++q) {
-    const int64_t j = tid + (int64_t)q * nthr;
-    if (j < nb) store_x_block(xr[q], xs + 12 * j);
+    const int j = tid + q * nthr;
+    if (j < nb) {
+      store_x_block(xr[q], xs + 12 * j);
+    } else if (j < xblocks) {
+      u32x4a* d = (u32x4a*)(xs + 12 * j);
+      d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
+    }
   }
-  if constexpr (LAYOUT != kNoWeights) {
-#pragma unroll
-    for (int q = 0; q < kTPer; ++q) {
-      const int e = tid + q * nthr;
-      if (e < 1024) {
-        LdsEntry t;
-        t.tlo = tr[q].x;
-        t.thi = tr[q].y;
-        t.factor = __builtin_bit_cast(float, (uint32_t)tr[q].z) * ((e >> 9) ? a.cen1 : a.cen0) * kTwo24;
-        t.nlev = tr[q].w & 0xFFu;
-        ts[e] = t;
-      }
+  if constexpr (kW) {
+    if (tid < kBallClasses) {
+      LdsEntry e;
+      e.tlo = tr.x;
+      e.thi = tr.y;
+      e.nlev = tr.w & 0xFFu;
+      const float f = __builtin_bit_cast(float, (uint32_t)tr.z) * kTwo24;
+      e.factor = f * a.cen0;
+      ts[tid] = e;
+      e.factor = f * a.cen1;
+      ts[tid + 512] = e;
     }
   }
   if constexpr (kUnits) {
@@ -600,35 +666,33 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   }
   __syncthreads();
 
-  auto tab = [&](uint32_t e) -> LdsEntry { return ts[e]; };
+  auto tab = [&](uint32_t e16) -> LdsEntry {
+    return *(const LdsEntry*)__builtin_assume_aligned((const uint8_t*)ts + e16, 16);
+  };
   auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
   auto cw = [&](uint32_t r) -> uint32_t { return cws[r]; };
+  const uint8_t* x_lane = (const uint8_t*)xs + cl * 48;
   float acc = 0.0f;
-  // One unit: decode slot pf[d] for unit g and accumulate.
-  // Lanes without a block decode their in-bounds stand-in and add 0.
-  auto process = [&](const Pref& p, int g) {
-    const LaneBlock b = unit_block(g);
-    const int j = g * a.C + (b.valid ? cl : 0);
-    const u32x4a* xp = (const u32x4a*)(xs + 12 * j);
+  // One unit: decode slot p for unit g and accumulate.
+  auto process = [&](const Pref& pr, int g, const Lane& L) {
+    const u32x4a* xp = (const u32x4a*)(x_lane + g * (C * 48));
     const u32x4a x0 = xp[0], x1 = xp[1], x2 = xp[2];
     const uint32_t xw[12] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w,
                              x2.x, x2.y, x2.z, x2.w};
     if constexpr (LAYOUT == kNoWeights) {
-      float s = 0.0f;
-#pragma unroll
-      for (int k = 0; k < 12; ++k) s = __builtin_amdgcn_fdot2(as_h2(0x3C003C00u), as_h2(xw[k]), s, false);
-      acc += b.valid ? s : 0.0f;
+      const uint32_t ones[12] = {0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u,
+                                 0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u,
+                                 0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
+      acc += dot12(ones, xw);
     } else {
-      uint32_t h[12], e;
-      decode_block<LAYOUT>(a, b, p, tab, g70, cw, side, h, e);
-      float s = 0.0f;
-#pragma unroll
-      for (int k = 0; k < 12; ++k) s = __builtin_amdgcn_fdot2(as_h2(h[k]), as_h2(xw[k]), s, false);
-      const float f = half_bits_to_float(p.scale) * ts[e].factor;
-      acc = __builtin_fmaf(s, b.valid ? f : 0.0f, acc);
+      uint32_t h[12], e16;
+      decode_block<LAYOUT>(pr, L.ul, tile, tile * groups + g, tab, g70, cw, side, a, h, e16);
+      const float s = dot12(h, xw);
+      acc = __builtin_fmaf((float)as_half(pr.scale), s * tab(e16).factor, acc);
     }
   };
-  const int units = (groups - wave + waves - 1) / waves;   // this wave's units
+  // this wave's full units: wave, wave + waves, ... < gf
+  const int units = wave < gf ? (gf - 1 - wave) / waves + 1 : 0;
   int done = 0;
   // Full rounds: consume every slot, refilling each with the unit kPrefetch
   // steps ahead (past the wave's last unit the refill is an in-bounds
@@ -640,45 +704,66 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
     for (int d = 0; d < kPrefetch; ++d) {
       const int g = wave + (done + d) * waves;
-      process(pf[d], g);
-      pf[d] = load_block<LAYOUT>(a, unit_block(g + kPrefetch * waves), side);
+      process(pf[d], g, Lp);
+      pf[d] = load_unit<LAYOUT, EVEN>(a, t, Lp, min(g + kPrefetch * waves, g_stand), side);
     }
   }
   // the last ≤ kPrefetch units are in flight: straight-line, no refills
 #pragma unroll
   for (int d = 0; d < kPrefetch; ++d)
-    if (d < units - done) process(pf[d], wave + (done + d) * waves);
-  for (int off = 1; off < a.C; off <<= 1) acc += __shfl_xor(acc, off);
+    if (d < units - done) process(pf[d], wave + (done + d) * waves, Lp);
+  // the last column group, by the wave next in turn; its lanes past the last
+  // column read zero x and add exactly zero
+  if (wave == gf % waves) process(plast, gf, Ll);
+  for (int off = 1; off < C; off <<= 1) acc += __shfl_xor(acc, off);
   if (cl == 0 && rl < R_t) red[wave * 64 + rl] = acc;
   __syncthreads();
   if (tid < R_t) {
     float y = 0.0f;
-    for (int w = 0; w < a.waves; ++w) y += red[w * 64 + tid];
+    for (int w = 0; w < waves; ++w) y += red[w * 64 + tid];
     a.y[(int64_t)tile * a.R + tid] = y;
   }
 }
 
 // --------------------------------------------------------- decode export
-// One thread per block, with the GEMV's own load and decode functions; the
-// binary16 pairs are turned back into integer coordinates (|z| in the low
-// byte of each half, the sign in its bit 15).
+// One thread per block, with the GEMV's decode function and plain loads at
+// the block's own byte offset; the binary16 pairs are turned back into integer
+// coordinates (|z| in the low byte of each half, the sign in its bit 15).
 template <int LAYOUT>
 __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, uint16_t* cout,
                                                      uint8_t* gout) {
   const int64_t bi = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (bi >= a.M * a.nb) return;
   const int64_t r = bi / a.nb, j = bi % a.nb;
-  const int64_t tile = r / a.R, g = j / a.C;
-  const int R_t = (int)min((int64_t)a.R, a.M - tile * a.R);
-  LaneBlock b = lane_block(a, tile, R_t, g, (int)(r % a.R), (int)(j % a.C));
-  b.loff = b.ul * Stride<LAYOUT>::v;
+  const int tile = (int)(r / a.R);
+  const int g = (int)(j / a.C);
+  const int R_t = (int)min((int64_t)a.R, a.M - (int64_t)tile * a.R);
+  const int C_g = (int)min((int64_t)a.C, a.nb - (int64_t)g * a.C);
+  const uint32_t ul = (uint32_t)((r % a.R) * C_g + (j % a.C));
+  const uint64_t blk = (uint64_t)tile * a.R * a.nb + (uint64_t)g * R_t * a.C + ul;
   const GlobalSide side{&a};
-  const Pref p = load_block<LAYOUT>(a, b, side);
-  auto tab = [&](uint32_t e) -> LdsEntry { return make_entry(a.table, e, 1.0f, 1.0f); };
+  Pref p = {0, 0, 0, 0, 0, 0, 0, 0};
+  if constexpr (LAYOUT == LEECH_SLOT32) {
+    uint64_t bits;
+    uint32_t base;
+    side.unit_entry(a.side0, tile * (int)a.groups + g, bits, base);
+    const uint32_t nbelow = (uint32_t)__builtin_popcountll(bits & ((1ull << ul) - 1ull));
+    const uint32_t* rec = (const uint32_t*)(a.main + (uint64_t)base * 4) +
+                          (ul * (uint32_t)kSlot32Small + nbelow * (uint32_t)(kSlot32Large - kSlot32Small)) / 4;
+    p.w0 = rec[0]; p.w1 = rec[1]; p.w2 = rec[2]; p.w3 = rec[3]; p.w4 = rec[4];
+  } else {
+    const uint64_t off = blk * Stride<LAYOUT>::v;
+    const uint32_t* w = (const uint32_t*)(a.main + (off & ~3ull));
+    p.w0 = w[0]; p.w1 = w[1]; p.w2 = w[2];
+    if constexpr (LAYOUT == LEECH_PLANES14) p.w3 = w[3];
+    p.sh = (uint32_t)(off & 3u) * 8u;
+    p.esh = (p.sh + 28u) & 31u;
+  }
+  auto tab = [&](uint32_t e16) -> LdsEntry { return make_entry(a.table, e16 >> 4, 1.0f, 1.0f); };
   auto g70 = [&](uint32_t c) -> G70Entry { return make_g70(a.table, c); };
   auto cw = [&](uint32_t rk) -> uint32_t { return a.codewords[rk]; };
-  uint32_t h[12], e;
-  decode_block<LAYOUT>(a, b, p, tab, g70, cw, side, h, e);
+  uint32_t h[12], e16;
+  decode_block<LAYOUT>(p, ul, tile, tile * (int)a.groups + g, tab, g70, cw, side, a, h, e16);
   int8_t z[kDim];
 #pragma unroll
   for (int k = 0; k < 12; ++k) {
@@ -695,6 +780,7 @@ __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, u
       zo[q] = (uint32_t)(uint8_t)z[4 * q] | (uint32_t)(uint8_t)z[4 * q + 1] << 8 |
               (uint32_t)(uint8_t)z[4 * q + 2] << 16 | (uint32_t)(uint8_t)z[4 * q + 3] << 24;
   }
+  const uint32_t e = e16 >> 4;
   if (cout) cout[bi] = (uint16_t)(e & 511u);
   if (gout) gout[bi] = (uint8_t)(e >> 9);
 }
@@ -751,6 +837,10 @@ static int check_desc_device(const leech_layout_desc* d) {
     return set_error(LEECH_E_SHAPE, "descriptor shape is not valid");
   if (d->lane_cols != choose_lane_cols(d->M))
     return set_error(LEECH_E_SHAPE, "descriptor lane_cols does not match its M");
+  // tile offsets (R·nb·20 bytes at most) and unit counts stay within 31 bits
+  if (d->M > (1ll << 31) || d->nb > (1ll << 24) ||
+      (uint64_t)(kWave / d->lane_cols) * (uint64_t)d->nb * 20u > 0x7FFFFFFFull)
+    return set_error(LEECH_E_SHAPE, "matrix too large for 32-bit tile offsets");
   return LEECH_OK;
 }
 
@@ -765,34 +855,49 @@ static GemvArgs make_args(const leech_layout_desc* d) {
   a.waves = waves_for(a.groups);
   a.tiles = (d->M + a.R - 1) / a.R;
   a.n_exc = d->n_exceptions;
+  a.main_bytes = d->main_bytes;
   return a;
+}
+
+// Every unit base of a fixed-stride layout is 4-aligned when the last tile's
+// units are (full tiles: 64 blocks per unit and a multiple of 4 rows per tile).
+static bool even_bases(const GemvArgs& a, int layout) {
+  const int64_t stride = layout == LEECH_PLANES14 ? kPlanes14Bytes
+                         : layout == LEECH_PLANES12X ? kPlanes12Bytes
+                         : layout == LEECH_GOLAY70 ? kGolay70Bytes : 0;
+  const int64_t rows_last = a.M - (a.tiles - 1) * a.R;
+  return (rows_last * a.C * stride) % 4 == 0;
 }
 
 template <int LAYOUT>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
-  const bool units = LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
-  const bool exc = LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
-  return (size_t)a.nb * 48 + (LAYOUT == kNoWeights ? 0 : 1024 * sizeof(LdsEntry)) +
+  return (size_t)a.groups * a.C * 48 +
          (LAYOUT == LEECH_GOLAY70 ? 512 * sizeof(G70Entry) + 4096 * 4 : 0) +
-         (units ? (size_t)a.groups * kUnitEntryBytes : 0) + (exc ? kExcLdsBytes : 0) +
-         (size_t)a.waves * 64 * 4;
+         (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
+         (has_exc<LAYOUT>() ? kExcLdsBytes : 0) + (size_t)a.waves * 64 * 4;
+}
+
+template <int LAYOUT, bool EVEN>
+static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
+  if (shmem + kTableBytes > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+    if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
+  }
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN>), dim3((unsigned)a.tiles), dim3(64 * a.waves),
+                     shmem, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail("gemv launch", e);
+  return LEECH_OK;
 }
 
 template <int LAYOUT>
 static int launch_gemv(const GemvArgs& a, hipStream_t st) {
   const size_t shmem = gemv_lds_bytes<LAYOUT>(a);
-  if (shmem > 160 * 1024)
+  if (shmem + kTableBytes > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
-  if (shmem > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
-    if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
-  }
-  const int64_t tiles = (a.M + a.R - 1) / a.R;
-  hipLaunchKernelGGL(gemv_kernel<LAYOUT>, dim3((unsigned)tiles), dim3(64 * a.waves), shmem, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail("gemv launch", e);
-  return LEECH_OK;
+  if (LAYOUT == kNoWeights || even_bases(a, LAYOUT)) return launch_gemv_as<LAYOUT, true>(a, shmem, st);
+  return launch_gemv_as<LAYOUT, false>(a, shmem, st);
 }
 
 template <int LAYOUT>
@@ -825,7 +930,8 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
   if (desc->layout == LEECH_GOLAY70 && !d_codewords)
     return set_error(LEECH_E_ARG, "GOLAY70 needs the codeword table");
   if (((uintptr_t)d_x & 15) || ((uintptr_t)d_main & 3) || ((uintptr_t)d_class_table & 15) ||
-      ((uintptr_t)d_codewords & 15) || ((uintptr_t)d_side0 & 3) || ((uintptr_t)d_side1 & 7))
+      ((uintptr_t)d_codewords & 15) || ((uintptr_t)d_side0 & 3) || ((uintptr_t)d_side1 & 7) ||
+      ((uintptr_t)d_scale & 1))
     return set_error(LEECH_E_ARG, "misaligned device pointer");
   GemvArgs a = make_args(desc);
   a.main = (const uint8_t*)d_main;

@@ -18,11 +18,17 @@ namespace leech {
 constexpr int kDim = 24;
 constexpr int kMaxLevels = 5;
 constexpr int kTableSlots = LEECH_TABLE_SLOTS;
+// Classes of the ball Λ24(12) (shells 2..12); the layouts only hold these ids.
+constexpr int kBallClasses = 301;
 constexpr int kWave = 64;
 constexpr int kPadBytes = 16;        // trailing zero bytes after every record stream
 
 // Record widths of the four layouts (bytes).
 constexpr int kPlanes14Bytes = 14;
+// Planes14 bit positions: planes p0, p1, p2 at 0, 32, 64, each followed by one
+// byte of the inverted sign mask; class (9 bits) and gain bit from bit 96.
+constexpr int kP14PlanePos[3] = {0, 32, 64};
+constexpr int kP14ClassPos = 96;
 constexpr int kPlanes12Bytes = 12;
 constexpr int kGolay70Bytes = 9;
 constexpr int kSlot32Small = 16;     // ≤ 4 levels
