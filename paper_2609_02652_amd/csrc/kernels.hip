@@ -358,6 +358,13 @@ struct TileCtx {
   __amdgpu_buffer_rsrc_t rec, sc;
   int tile, R_t, C, groups;
 };
+// A descriptor with no records: every load through it is out of range, returns
+// zeros and reaches no memory.  Loads whose data is not needed (stand-in units,
+// staging loads of waves with nothing to stage) go through it, so every wave
+// issues the same load sequence without the bytes.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t null_rsrc() {
+  return __builtin_amdgcn_make_buffer_rsrc(nullptr, 0, 0, kRsrcWord3);
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t bytes) {
   const uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
@@ -366,12 +373,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 
 // Loads of unit g for a lane at place L.  EVEN: every unit base of the layout
 // is 4-aligned, so L is used as is; otherwise the lane's window is recomputed
-// from the unit base's offset modulo 4.  Loads are issued unconditionally
-// (callers hand in an in-bounds stand-in unit and ignore its data): branches
-// around loads would make the compiler's wait counts conservative.
+// from the unit base's offset modulo 4.  Loads are issued unconditionally:
+// branches around loads would make the compiler's wait counts conservative.
+// For a unit whose data is not needed (live = false, wave-uniform) the loads go
+// through the null descriptor; g must still be a real unit (Slot32 reads its
+// record pointer from the unit's side entry).
 template <int LAYOUT, bool EVEN, class SIDE>
-__device__ __forceinline__ Pref load_unit(const GemvArgs& a, const TileCtx& t, const Lane& L, int g,
-                                          const SIDE& side) {
+__device__ __forceinline__ Pref load_unit(const GemvArgs& a, const TileCtx& t, bool live,
+                                          const Lane& L, int g, const SIDE& side) {
   Pref p = {0, 0, 0, 0, 0, 0, 0, 0};
   if constexpr (LAYOUT == kNoWeights) {
     return p;
@@ -394,16 +403,19 @@ __device__ __forceinline__ Pref load_unit(const GemvArgs& a, const TileCtx& t, c
       if constexpr (!EVEN) l = lane_place(L.ul, S, ub & 3u);
       const int soff = (int)(ub & ~3u);
       if constexpr (LAYOUT == LEECH_PLANES14) {
-        const u32x4a w = __builtin_amdgcn_raw_buffer_load_b128(t.rec, (int)l.rec, soff, kStreamed);
+        const u32x4a w = __builtin_amdgcn_raw_buffer_load_b128(live ? t.rec : null_rsrc(), (int)l.rec,
+                                                               soff, kStreamed);
         p.w0 = w.x; p.w1 = w.y; p.w2 = w.z; p.w3 = w.w;
       } else {
-        const u32x3 w = __builtin_amdgcn_raw_buffer_load_b96(t.rec, (int)l.rec, soff, kStreamed);
+        const u32x3 w = __builtin_amdgcn_raw_buffer_load_b96(live ? t.rec : null_rsrc(), (int)l.rec,
+                                                             soff, kStreamed);
         p.w0 = w.x; p.w1 = w.y; p.w2 = w.z;
       }
       p.sh = l.sh;
       p.esh = l.esh;
     }
-    p.scale = __builtin_amdgcn_raw_buffer_load_b16(t.sc, (int)(L.ul * 2u), (int)(blk * 2u), kStreamed);
+    p.scale = __builtin_amdgcn_raw_buffer_load_b16(live ? t.sc : null_rsrc(), (int)(L.ul * 2u),
+                                                   (int)(blk * 2u), kStreamed);
     return p;
   }
 }
@@ -521,8 +533,11 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const int C_last = (int)(nb - (int64_t)gf * C);
   const bool row_ok = rl < R_t, last_ok = row_ok && cl < C_last;
   constexpr uint32_t S = Stride<LAYOUT>::v;
-  const Lane Lf = lane_place(row_ok ? (uint32_t)(rl * C + cl) : 0u, S, 0u);
-  const Lane Ll = lane_place(last_ok ? (uint32_t)(rl * C_last + cl) : 0u, S, 0u);
+  // 24-bit products: a 64-bit multiply-add chosen for these would read an
+  // undefined high half that may sit in a register with a load in flight, and
+  // the wait for it drains every outstanding load
+  const Lane Lf = lane_place(row_ok ? __umul24(rl, C) + cl : 0u, S, 0u);
+  const Lane Ll = lane_place(last_ok ? __umul24(rl, C_last) + cl : 0u, S, 0u);
   // the pipeline's lane place and its stand-in unit: a full unit when there is
   // one, else the last (then the pipeline processes nothing)
   const Lane Lp = gf > 0 ? Lf : Ll;
@@ -600,14 +615,26 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     if (side.exc_in_lds)
       for (int64_t c = tid + (int64_t)kEPer * nthr; c < (int64_t)exc_chunks; c += nthr)
         ((u32x4a*)exc_lds)[c] = ((const u32x4a*)(a.side0 + side.exc_start))[c];
+  // x and the class table through buffer descriptors: a wave with no block
+  // (no class) to stage loads through the null descriptor, and lanes past nb
+  // read zeros, which is the padding past the last column
+  const __amdgpu_buffer_rsrc_t rs_x = make_rsrc(a.x, (uint64_t)nb * 48);
   XBlock xr[kXPer];
 #pragma unroll
   for (int q = 0; q < kXPer; ++q) {
-    const int64_t j = min(tid + (int64_t)q * nthr, nb - 1);    // clamped: loads stay unconditional
-    xr[q] = load_x_block(a.x + 24 * j);
+    const bool live = q * nthr + wave * 64 < nb;
+    const int off = (tid + q * nthr) * 48;
+    const __amdgpu_buffer_rsrc_t r = live ? rs_x : null_rsrc();
+    xr[q].v0 = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    xr[q].v1 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
+    xr[q].v2 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 32, 0, 0);
   }
   u32x4a tr = {0, 0, 0, 0};
-  if constexpr (kW) tr = *(const u32x4a*)&a.table[min(tid, kBallClasses - 1)];
+  if constexpr (kW) {
+    const __amdgpu_buffer_rsrc_t r =
+        wave * 64 < kBallClasses ? make_rsrc(a.table, kBallClasses * sizeof(DevClass)) : null_rsrc();
+    tr = __builtin_amdgcn_raw_buffer_load_b128(r, tid * (int)sizeof(DevClass), 0, 0);
+  }
   u32x4a ur[kUPer], er[kEPer];
   if constexpr (kUnits) {
 #pragma unroll
@@ -622,22 +649,21 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
                                                                   (int64_t)exc_chunks - 1)];
     }
   }
-  const Pref plast = load_unit<LAYOUT, EVEN>(a, t, Ll, gf, gside);
+  // the last column group: only its wave needs the data
+  const int w_last = gf % waves;
+  const Pref plast = load_unit<LAYOUT, EVEN>(a, t, wave == w_last, Ll, gf, gside);
+  // this wave's full units: wave, wave + waves, ... < gf
+  const int units = wave < gf ? (gf - 1 - wave) / waves + 1 : 0;
   Pref pf[kPrefetch];
 #pragma unroll
   for (int d = 0; d < kPrefetch; ++d) {
-    pf[d] = load_unit<LAYOUT, EVEN>(a, t, Lp, min(wave + d * waves, g_stand), gside);
+    pf[d] = load_unit<LAYOUT, EVEN>(a, t, d < units, Lp, min(wave + d * waves, g_stand), gside);
     __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
   }
 #pragma unroll
   for (int q = 0; q < kXPer; ++q) {
     const int j = tid + q * nthr;
-    if (j < nb) {
-      store_x_block(xr[q], xs + 12 * j);
-    } else if (j < xblocks) {
-      u32x4a* d = (u32x4a*)(xs + 12 * j);
-      d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
-    }
+    if (j < xblocks) store_x_block(xr[q], xs + 12 * j);
   }
   if constexpr (kW) {
     if (tid < kBallClasses) {
@@ -671,7 +697,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   };
   auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
   auto cw = [&](uint32_t r) -> uint32_t { return cws[r]; };
-  const uint8_t* x_lane = (const uint8_t*)xs + cl * 48;
+  const uint8_t* x_lane = (const uint8_t*)xs + __umul24(cl, 48u);
   float acc = 0.0f;
   // One unit: decode slot p for unit g and accumulate.
   auto process = [&](const Pref& pr, int g, const Lane& L) {
@@ -691,8 +717,6 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       acc = __builtin_fmaf((float)as_half(pr.scale), s * tab(e16).factor, acc);
     }
   };
-  // this wave's full units: wave, wave + waves, ... < gf
-  const int units = wave < gf ? (gf - 1 - wave) / waves + 1 : 0;
   int done = 0;
   // Full rounds: consume every slot, refilling each with the unit kPrefetch
   // steps ahead (past the wave's last unit the refill is an in-bounds
@@ -705,7 +729,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     for (int d = 0; d < kPrefetch; ++d) {
       const int g = wave + (done + d) * waves;
       process(pf[d], g, Lp);
-      pf[d] = load_unit<LAYOUT, EVEN>(a, t, Lp, min(g + kPrefetch * waves, g_stand), side);
+      pf[d] = load_unit<LAYOUT, EVEN>(a, t, done + d + kPrefetch < units, Lp,
+                                      min(g + kPrefetch * waves, g_stand), side);
     }
   }
   // the last ≤ kPrefetch units are in flight: straight-line, no refills
@@ -714,7 +739,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     if (d < units - done) process(pf[d], wave + (done + d) * waves, Lp);
   // the last column group, by the wave next in turn; its lanes past the last
   // column read zero x and add exactly zero
-  if (wave == gf % waves) process(plast, gf, Ll);
+  if (wave == w_last) process(plast, gf, Ll);
   for (int off = 1; off < C; off <<= 1) acc += __shfl_xor(acc, off);
   if (cl == 0 && rl < R_t) red[wave * 64 + rl] = acc;
   __syncthreads();
