@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-layer", action="store_true",
+                    help="skip the 8B-layer comparison (separate vs fused launches vs FP16)")
+    ap.add_argument("--layer-steps", type=int, default=300)
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -139,6 +142,120 @@ def time_arm(torch, arm, steps):
     e1.record(st)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1)
+
+
+# One 8B-class decoder layer at batch 1: (name, rows, K), K padded to 24.
+LAYER_8B = [("q", 4096, 4096), ("k", 1024, 4096), ("v", 1024, 4096), ("o", 4096, 4096),
+            ("gate", 14336, 4096), ("up", 14336, 4096), ("down", 4096, 14336)]
+FUSED_8B = [("qkv", ["q", "k", "v"]), ("o", ["o"]), ("gate_up", ["gate", "up"]), ("down", ["down"])]
+
+
+def bench_layer(args, torch, P, synth):
+    """µs per decoder layer: seven Planes14 GEMVs, the same weights in four
+    fused launches (q/k/v and gate/up row-concatenated, §3.4), and seven FP16
+    GEMVs; each timed as one graph replay of args.layer_steps layers walking
+    ≥ 1 GiB of replicas."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    cb = P.Codebook(12)
+    dcb = P.DeviceCodebook(cb, dev)
+    t0 = time.time()
+    parts = {}
+    for i, (name, M, K) in enumerate(LAYER_8B):
+        inp = synth.make_gemv_inputs(M, K, seed=1000 + i, name=f"layer8b-{name}")
+        parts[name] = inp
+    log(f"[bench] 8B layer inputs ready in {time.time() - t0:.1f}s")
+    xs = {K: torch.from_numpy(synth.make_activation(K, seed=1, name=f"layer8b-x{K}")).to(dev)
+          for K in {K for _, _, K in LAYER_8B}}
+    cen = (1.0, 1.0)
+
+    def xfor(inp):
+        return xs[inp.K]
+
+    def leech(names):
+        z = np.concatenate([parts[n].z for n in names])
+        gain = np.concatenate([parts[n].gain for n in names])
+        scale = np.concatenate([parts[n].scale for n in names])
+        cls, sm, lv = cb.fields_from_points(z)
+        return P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, gain, sm, lv, scale, dev)
+
+    sep = {n: leech([n]) for n, _, _ in LAYER_8B}
+    fused = {f: (leech(ns), [parts[n].M for n in ns]) for f, ns in FUSED_8B}
+    layer_bytes = sum(m.desc.served_bytes for m in sep.values())
+    reps = max(1, math.ceil(REPLICA_BYTES / layer_bytes))
+
+    def clone(m):
+        return P.LeechMatrix(m.desc, m.main.clone(), m.side0.clone(), m.side1.clone(),
+                             m.scale.clone(), dcb)
+
+    ys = {n: torch.empty(parts[n].M, dtype=torch.float32, device=dev) for n in parts}
+    yf = {f: torch.empty(sum(r), dtype=torch.float32, device=dev) for f, (_, r) in fused.items()}
+    sep_r = [sep] + [{n: clone(m) for n, m in sep.items()} for _ in range(reps - 1)]
+    fus_r = [fused] + [{f: (clone(m), r) for f, (m, r) in fused.items()} for _ in range(reps - 1)]
+
+    def run_sep(i):
+        for n, m in sep_r[i % reps].items():
+            m.gemv(xfor(parts[n]), ys[n], centroids=cen)
+
+    def run_fused(i):
+        for f, (m, rows) in fus_r[i % reps].items():
+            m.gemv_grouped(xfor(parts[dict(FUSED_8B)[f][0]]), rows, [cen] * len(rows), yf[f])
+
+    # FP16 arm: the same layer as binary16 weights (decoded on the device)
+    fp = {}
+    for n, m in sep.items():
+        z, _, _ = m.decode()
+        zf = z.float()
+        inp = parts[n]
+        fac = torch.from_numpy(inp.scale.astype("float32")).to(dev) / zf.pow(2).sum(-1).sqrt()
+        fp[n] = (zf * fac[..., None]).reshape(inp.M, inp.Kpad).half().contiguous()
+        del z, zf
+    fp_bytes = sum(w.numel() * 2 for w in fp.values())
+    fp_reps = max(1, math.ceil(REPLICA_BYTES / fp_bytes))
+    fp_r = [fp] + [{n: w.clone() for n, w in fp.items()} for _ in range(fp_reps - 1)]
+
+    def run_fp(i):
+        for n, w in fp_r[i % fp_reps].items():
+            P.fp16_gemv(w, xfor(parts[n]), ys[n])
+
+    # outputs agree (fused rows are the separate rows, within f32 rounding)
+    run_sep(0)
+    run_fused(0)
+    torch.cuda.synchronize()
+    ysep = torch.cat([ys[n] for n in ("q", "k", "v")])
+    rel = float(((yf["qkv"] - ysep).abs().max() / ysep.abs().max()).item())
+    res = {}
+    for name, fn, nrep in (("separate", run_sep, reps), ("fused", run_fused, reps),
+                           ("fp16", run_fp, fp_reps)):
+        steps = args.layer_steps
+        g = torch.cuda.CUDAGraph()
+        fn(0)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            for i in range(steps):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        meds = []
+        for _ in range(3):
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            meds.append(e0.elapsed_time(e1) * 1e3 / steps)
+        res[name] = round(statistics.median(meds), 2)
+        log(f"[bench] 8B layer {name}: {res[name]} us/layer ({nrep} replicas)")
+        del g
+    return {"workload": "one 8B-class decoder layer at batch 1 (q, o 4096x4104; k, v 1024x4104; "
+                        "gate, up 14336x4104; down 4096x14352), Planes14",
+            "served_bytes": layer_bytes, "us_separate_7_launches": res["separate"],
+            "us_fused_4_launches": res["fused"], "us_fp16_7_launches": res["fp16"],
+            "fusion_saves": round(1 - res["fused"] / res["separate"], 4),
+            "fused_vs_fp16": round(res["fp16"] / res["fused"], 3),
+            "fused_GBps": round(layer_bytes / (res["fused"] * 1e-6) / 1e9, 1),
+            "qkv_fused_vs_separate_max_rel_diff": rel}
 
 
 def measured_traffic(config):
@@ -245,6 +362,13 @@ def main():
             row["vs_fp16"] = round(statistics.median(ratios), 3)
         table[n] = row
 
+    layer = None
+    if not args.no_layer:
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        layer = bench_layer(args, torch, P, synth)
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f}s")
@@ -274,6 +398,7 @@ def main():
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config)},
         "arms": table,
+        "layer_8b": layer,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -193,6 +193,22 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
                const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
                float* d_y, void* stream);
 
+/* Row-grouped GEMV (§3.4: q/k/v and gate/up fused into row-concatenated
+ * launches): W is the row concatenation of n_groups matrices sharing one
+ * activation, expanded as one layout of M = Σ group_rows rows; group g's rows
+ * use the gain centroids group_centroids[2g], group_centroids[2g + 1].
+ * group_rows and group_centroids are host arrays; every group boundary must
+ * be a multiple of 64 rows (so no wave tile straddles two groups).  Other
+ * arguments as leech_gemv.  1 ≤ n_groups ≤ LEECH_MAX_GROUPS; LEECH_E_SHAPE if
+ * the rows do not sum to M or a boundary is misplaced, LEECH_E_ARG for a
+ * non-finite centroid. */
+#define LEECH_MAX_GROUPS 8
+int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                       const void* d_side1, const void* d_class_table, const void* d_codewords,
+                       const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
+                       const float* group_centroids, const uint16_t* d_x, float* d_y,
+                       void* stream);
+
 /* Verification decode on the device with the GEMV's own decoders: z int8
  * [M·nb][24], class_id [M·nb], gain_bit [M·nb], row-major (r, j).  Any output
  * may be NULL. */

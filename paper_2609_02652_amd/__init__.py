@@ -89,6 +89,23 @@ class LeechMatrix:
                   self.scale.data_ptr(), centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
         return y
 
+    def gemv_grouped(self, x, group_rows, group_centroids, y=None, stream=None):
+        """y = W x for a row concatenation of matrices sharing x (§3.4): group g
+        covers the next group_rows[g] rows and uses gain centroids
+        group_centroids[g] = (c0, c1); group boundaries are multiples of 64 rows."""
+        torch = _torch()
+        if x.dtype != torch.float16 or x.numel() != self.Kpad or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 tensor of length Kpad")
+        if y is None:
+            y = torch.empty(self.M, dtype=torch.float32, device=x.device)
+        elif y.dtype != torch.float32 or y.numel() != self.M or not y.is_contiguous():
+            raise ValueError("y must be a contiguous f32 tensor of length M")
+        m, s0, s1 = self._ptrs()
+        _lib.gemv_grouped(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
+                          self.dcb.codewords.data_ptr(), self.scale.data_ptr(), group_rows,
+                          group_centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
+        return y
+
     def decode(self, stream=None):
         """Device decode: (z int8 [M, nb, 24], class_id int16 [M, nb], gain uint8 [M, nb])."""
         torch = _torch()

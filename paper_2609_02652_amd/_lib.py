@@ -24,7 +24,7 @@ ERRORS = {0: "OK", -1: "LEECH_E_ARG", -2: "LEECH_E_LAYOUT", -3: "LEECH_E_SHAPE",
 EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_codebook_info", "leech_codebook_class", "leech_codebook_table",
            "leech_fields_from_points", "leech_expand_layout", "leech_layout_scales",
-           "leech_host_decode_layout", "leech_gemv", "leech_decode_blocks",
+           "leech_host_decode_layout", "leech_gemv", "leech_gemv_grouped", "leech_decode_blocks",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl"]
 
 
@@ -66,6 +66,7 @@ def _load() -> C.CDLL:
         "leech_layout_scales": (I, [C.POINTER(LayoutDesc), P, P]),
         "leech_host_decode_layout": (I, [P, C.POINTER(LayoutDesc), P, P, P, P, P, P]),
         "leech_gemv": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P, P]),
+        "leech_gemv_grouped": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, I, P, P, P, P, P]),
         "leech_decode_blocks": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P]),
         "leech_fp16_gemv_ref": (I, [I64, I64, P, P, P, P]),
         "leech_noweights_ctrl": (I, [C.POINTER(LayoutDesc), P, P, P]),
@@ -189,6 +190,20 @@ def gemv(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroid
     check(lib.leech_gemv(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
                          d_codewords or None, d_scale, C.cast(cen, C.c_void_p), d_x, d_y,
                          stream or None))
+
+
+MAX_GROUPS = 8
+
+
+def gemv_grouped(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, group_rows,
+                 group_centroids, d_x, d_y, stream=0):
+    n = len(group_rows)
+    rows = (C.c_int64 * max(n, 1))(*[int(r) for r in group_rows])
+    cen = (C.c_float * max(2 * n, 2))(*[float(c) for pair in group_centroids for c in pair])
+    check(lib.leech_gemv_grouped(C.byref(desc), d_main, d_side0 or None, d_side1 or None,
+                                 d_table, d_codewords or None, d_scale, n,
+                                 C.cast(rows, C.c_void_p), C.cast(cen, C.c_void_p), d_x, d_y,
+                                 stream or None))
 
 
 def decode_blocks(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_z, d_cls, d_gain,

@@ -40,6 +40,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -90,6 +91,10 @@ struct GemvArgs {
   int64_t tiles;
   uint64_t n_exc;               // exception records (Planes12x, Golay70)
   uint64_t main_bytes;
+  // row groups with their own gain centroids (0: one group, cen0/cen1)
+  int ngroups;
+  int64_t grp_end[LEECH_MAX_GROUPS];      // first row past each group
+  float grp_cen[LEECH_MAX_GROUPS][2];
 };
 
 // Where side data comes from: global memory (verification decode, and the
@@ -598,10 +603,19 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
     }
   }
+  // the tile's gain centroids: its row group's (tiles never straddle groups)
+  float cen0 = a.cen0, cen1 = a.cen1;
+  if (a.ngroups > 0) {
+    const int64_t row0 = (int64_t)tile * a.R;
+    int gi = 0;
+    while (gi < a.ngroups - 1 && row0 >= a.grp_end[gi]) ++gi;
+    cen0 = a.grp_cen[gi][0];
+    cen1 = a.grp_cen[gi][1];
+  }
   if constexpr (kW)
     for (int c = tid + nthr; c < kBallClasses; c += nthr) {
-      ts[c] = make_entry(a.table, (uint32_t)c, a.cen0, a.cen1);
-      ts[c + 512] = make_entry(a.table, (uint32_t)c | 512u, a.cen0, a.cen1);
+      ts[c] = make_entry(a.table, (uint32_t)c, cen0, cen1);
+      ts[c + 512] = make_entry(a.table, (uint32_t)c | 512u, cen0, cen1);
     }
   if constexpr (LAYOUT == LEECH_GOLAY70) {
     for (int c = tid; c < 512; c += nthr) gs[c] = make_g70(a.table, (uint32_t)c);
@@ -672,9 +686,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       e.thi = tr.y;
       e.nlev = tr.w & 0xFFu;
       const float f = __builtin_bit_cast(float, (uint32_t)tr.z) * kTwo24;
-      e.factor = f * a.cen0;
+      e.factor = f * cen0;
       ts[tid] = e;
-      e.factor = f * a.cen1;
+      e.factor = f * cen1;
       ts[tid + 512] = e;
     }
   }
@@ -935,20 +949,14 @@ static int launch_decode(const GemvArgs& a, int8_t* z, uint16_t* c, uint8_t* g, 
   return LEECH_OK;
 }
 
-}  // namespace leech
-
-using namespace leech;
-
-extern "C" {
-
-int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
-               const void* d_side1, const void* d_class_table, const void* d_codewords,
-               const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
-               float* d_y, void* stream) {
-  clear_error();
+// Validation and argument setup shared by the GEMV entry points; the caller
+// fills the centroids.
+static int gemv_setup(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                      const void* d_side1, const void* d_class_table, const void* d_codewords,
+                      const uint16_t* d_scale, const uint16_t* d_x, float* d_y, GemvArgs* out) {
   int rc = check_desc_device(desc);
   if (rc) return rc;
-  if (!d_main || !d_class_table || !d_scale || !centroid || !d_x || !d_y)
+  if (!d_main || !d_class_table || !d_scale || !d_x || !d_y)
     return set_error(LEECH_E_ARG, "NULL argument");
   if ((desc->side_bytes[0] && !d_side0) || (desc->side_bytes[1] && !d_side1))
     return set_error(LEECH_E_ARG, "layout needs its side streams");
@@ -967,9 +975,11 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
   a.scale = d_scale;
   a.x = d_x;
   a.y = d_y;
-  a.cen0 = centroid[0];
-  a.cen1 = centroid[1];
-  hipStream_t st = (hipStream_t)stream;
+  *out = a;
+  return LEECH_OK;
+}
+
+static int gemv_dispatch(const leech_layout_desc* desc, const GemvArgs& a, hipStream_t st) {
   switch (desc->layout) {
     case LEECH_SLOT32: return launch_gemv<LEECH_SLOT32>(a, st);
     case LEECH_PLANES14: return launch_gemv<LEECH_PLANES14>(a, st);
@@ -977,6 +987,59 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
     case LEECH_GOLAY70: return launch_gemv<LEECH_GOLAY70>(a, st);
     default: return set_error(LEECH_E_LAYOUT, "unknown layout");
   }
+}
+}  // namespace leech
+
+using namespace leech;
+
+extern "C" {
+
+int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+               const void* d_side1, const void* d_class_table, const void* d_codewords,
+               const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
+               float* d_y, void* stream) {
+  clear_error();
+  if (!centroid) return set_error(LEECH_E_ARG, "NULL argument");
+  GemvArgs a;
+  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_x,
+                      d_y, &a);
+  if (rc) return rc;
+  a.cen0 = centroid[0];
+  a.cen1 = centroid[1];
+  return gemv_dispatch(desc, a, (hipStream_t)stream);
+}
+
+int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                       const void* d_side1, const void* d_class_table, const void* d_codewords,
+                       const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
+                       const float* group_centroids, const uint16_t* d_x, float* d_y,
+                       void* stream) {
+  clear_error();
+  if (!group_rows || !group_centroids) return set_error(LEECH_E_ARG, "NULL argument");
+  if (n_groups < 1 || n_groups > LEECH_MAX_GROUPS)
+    return set_error(LEECH_E_ARG, "n_groups must be 1.." + std::to_string(LEECH_MAX_GROUPS));
+  GemvArgs a;
+  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_x,
+                      d_y, &a);
+  if (rc) return rc;
+  int64_t end = 0;
+  for (int g = 0; g < n_groups; ++g) {
+    if (group_rows[g] <= 0) return set_error(LEECH_E_SHAPE, "every group needs rows");
+    end += group_rows[g];
+    if (g + 1 < n_groups && end % kWave)
+      return set_error(LEECH_E_SHAPE, "group boundaries must be multiples of 64 rows");
+    const float c0 = group_centroids[2 * g], c1 = group_centroids[2 * g + 1];
+    if (!std::isfinite(c0) || !std::isfinite(c1))
+      return set_error(LEECH_E_ARG, "group centroids must be finite");
+    a.grp_end[g] = end;
+    a.grp_cen[g][0] = c0;
+    a.grp_cen[g][1] = c1;
+  }
+  if (end != desc->M) return set_error(LEECH_E_SHAPE, "group rows do not sum to M");
+  a.ngroups = n_groups;
+  a.cen0 = a.grp_cen[0][0];
+  a.cen1 = a.grp_cen[0][1];
+  return gemv_dispatch(desc, a, (hipStream_t)stream);
 }
 
 int leech_decode_blocks(const leech_layout_desc* desc, const void* d_main, const void* d_side0,

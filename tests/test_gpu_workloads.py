@@ -100,3 +100,68 @@ def test_odd_last_tile_all_layouts(dev, dcb):
     """lane_cols 1 with a one-row last tile: unit bases that are not 4-aligned."""
     check_matrix(dev, dcb, "tall-odd", 16385, 24 * 5, seed=7,
                  layouts=("planes14", "slot32", "planes12x", "golay70"), rows_sampled=256)
+
+
+# ----------------------------------------------------------- fused launches
+def fused_inputs(parts, seed0):
+    """Row concatenation of independently drawn matrices sharing one K (and x)."""
+    ins = [synth.make_gemv_inputs(M, K, seed=seed0 + i, name=f"fused{i}")
+           for i, (M, K) in enumerate(parts)]
+    x = ins[0].x
+    cat = lambda f: np.concatenate([getattr(i, f) for i in ins], axis=0)  # noqa: E731
+    return ins, cat("z"), cat("gain"), cat("scale"), x
+
+
+def check_fused(dev, dcb, parts, cens, seed0, layouts, rows_per_part=None):
+    ins, z, gain, scale, x = fused_inputs(parts, seed0)
+    cls, sm, lv = dcb.cb.fields_from_points(z)
+    xt = torch.from_numpy(x).to(dev)
+    group_rows = [M for M, _ in parts]
+    ref_bits = None
+    for lay in layouts:
+        say(f"[fused] parts={parts} layout={lay}")
+        mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[lay], cls, gain, sm, lv, scale, dev)
+        y = mat.gemv_grouped(xt, group_rows, cens).cpu().numpy()
+        r0 = 0
+        for i, (inp, c) in enumerate(zip(ins, cens)):
+            M = inp.M
+            rows = np.arange(M) if rows_per_part is None else \
+                np.sort(np.random.default_rng(i).choice(M, min(rows_per_part, M), replace=False))
+            sub = synth.GemvInputs(len(rows), inp.K, inp.Kpad, inp.nb, inp.z[rows], inp.gain[rows],
+                                   inp.scale[rows], x, inp.seed, inp.name)
+            W = D.weights64_from_points(sub.z, sub.gain, sub.scale, c)
+            e = D.errors(y[r0 + rows], D.gemv64(W, x), W, x)
+            say(f"    group {i} ({M} rows, centroids {c}): {e}")
+            assert e["max_norm_err"] <= TOL_NORM and e["max_abs_err"] <= TOL_PAPER
+            r0 += M
+        if ref_bits is None:
+            ref_bits = y.view(np.uint32).copy()
+        assert (y.view(np.uint32) == ref_bits).all(), f"{lay} not bit-identical"
+        del mat
+        torch.cuda.empty_cache()
+
+
+def test_fused_qkv_small_all_layouts(dev, dcb):
+    check_fused(dev, dcb, [(256, 408), (64, 408), (64, 408)],
+                [(0.75, 1.25), (0.9, 1.1), (1.3, 0.6)], seed0=300,
+                layouts=("planes14", "slot32", "planes12x", "golay70"))
+
+
+def test_fused_layer_8b(dev, dcb):
+    """q/k/v in one launch and gate/up in one launch, as served (Planes14)."""
+    check_fused(dev, dcb, [(4096, 4096), (1024, 4096), (1024, 4096)],
+                [(0.75, 1.25), (0.9, 1.1), (1.3, 0.6)], seed0=400, layouts=("planes14",),
+                rows_per_part=64)
+    check_fused(dev, dcb, [(14336, 4096), (14336, 4096)], [(0.8, 1.2), (1.1, 0.95)], seed0=500,
+                layouts=("planes14",), rows_per_part=64)
+
+
+def test_fused_single_group_matches_plain_gemv(dev, dcb):
+    """One group with the plain call's centroids gives the plain call's bits."""
+    inp = synth.make_gemv_inputs(768, 1536, seed=9, name="one-group")
+    cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+    mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    x = torch.from_numpy(inp.x).to(dev)
+    a = mat.gemv(x, centroids=CEN).cpu().numpy()
+    b = mat.gemv_grouped(x, [768], [CEN]).cpu().numpy()
+    assert (a.view(np.uint32) == b.view(np.uint32)).all()

@@ -191,6 +191,27 @@ def test_device_calls_validate_before_launch():
     assert e.value.code == -1
 
 
+def test_grouped_gemv_validates_groups_before_launch():
+    """Row groups are checked on the host; every case here fails before any
+    launch (the device pointers are stand-ins that are never dereferenced)."""
+    d = P.LayoutDesc()
+    d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 128, 48, 2
+    d.lane_cols = 16                     # what the library picks for M = 128
+    fake = 256
+    cases = [
+        ([], [], -1),                                 # no group
+        ([16] * 8 + [0], [(1, 1)] * 9, -1),           # more than 8 groups
+        ([64, 32], [(1, 1), (1, 1)], -3),             # rows do not sum to M
+        ([32, 96], [(1, 1), (1, 1)], -3),             # boundary not on 64 rows
+        ([64, 64], [(1, float("nan")), (1, 1)], -1),  # non-finite centroid
+        ([64, 0, 64], [(1, 1)] * 3, -3),              # empty group
+    ]
+    for rows, cens, code in cases:
+        with pytest.raises(P.LeechError) as e:
+            _lib.gemv_grouped(d, fake, 0, 0, fake, 0, fake, rows, cens, fake, fake)
+        assert e.value.code == code, (rows, cens, _lib.lib.leech_last_error())
+
+
 def test_lane_cols_fill_the_gpu():
     from paper_2609_02652_amd._lib import LayoutDesc  # noqa: F401
     cases = {768: 16, 1024: 16, 4096: 4, 8192: 2, 14336: 2, 16384: 1, 17408: 1}
