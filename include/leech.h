@@ -230,6 +230,20 @@ int leech_fp16_gemv_ref(int64_t M, int64_t K, const uint16_t* d_W, const uint16_
 int leech_noweights_ctrl(const leech_layout_desc* desc, const uint16_t* d_x, float* d_y,
                          void* stream);
 
+/* Activation rotation (§2.3 "The kernel", §6 "The rotated basis"): weights
+ * live in a rotated basis, so the activation is rotated before the GEMV.  For
+ * K = n·m with n = 2^k the largest power of two dividing K (n ≤ 32768), every
+ * block b of n consecutive coordinates becomes
+ *     xr[b·n + i] = n^(-1/2) · Σ_j H_n[i][j] · s[b·n + j] · x[b·n + j],
+ * H_n[i][j] = (−1)^popcount(i & j) (Sylvester-ordered Walsh–Hadamard), with s
+ * the caller's ±1 signs (int8 [K]; NULL = all +1).  d_x: binary16 [K];
+ * d_xr: binary16 [Kpad], the f32 result rounded to nearest even, zero past K,
+ * ready as the GEMV's activation; d_xr32: optional f32 [K] copy of the values
+ * before that rounding (NULL to skip).  Arithmetic in f32.  LEECH_E_SHAPE if
+ * K ≤ 0, Kpad < K or n > 32768. */
+int leech_rotate_x(int64_t K, int64_t Kpad, const uint16_t* d_x, const int8_t* d_signs,
+                   uint16_t* d_xr, float* d_xr32, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

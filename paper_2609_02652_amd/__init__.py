@@ -140,3 +140,22 @@ def noweights_ctrl(desc: LayoutDesc, x, y=None, stream=None):
         y = torch.empty(desc.M, dtype=torch.float32, device=x.device)
     _lib.noweights_ctrl(desc, x.data_ptr(), y.data_ptr(), _stream(stream))
     return y
+
+
+def rotate_x(x, signs=None, Kpad=None, with_f32=False, stream=None):
+    """Blockwise Walsh–Hadamard rotation of an fp16 activation (§2.3, §6):
+    x fp16 [K], signs int8 ±1 [K] (None: all +1) -> fp16 [Kpad] (zero past K),
+    and the f32 values before rounding when with_f32."""
+    torch = _torch()
+    if x.dtype != torch.float16 or x.dim() != 1 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous 1-D fp16 tensor")
+    K = x.numel()
+    Kpad = K if Kpad is None else int(Kpad)
+    if signs is not None and (signs.dtype != torch.int8 or signs.numel() != K
+                              or not signs.is_contiguous()):
+        raise ValueError("signs must be a contiguous int8 tensor of length K")
+    xr = torch.empty(Kpad, dtype=torch.float16, device=x.device)
+    xr32 = torch.empty(K, dtype=torch.float32, device=x.device) if with_f32 else None
+    _lib.rotate_x(K, Kpad, x.data_ptr(), signs.data_ptr() if signs is not None else 0,
+                  xr.data_ptr(), xr32.data_ptr() if with_f32 else 0, _stream(stream))
+    return (xr, xr32) if with_f32 else xr

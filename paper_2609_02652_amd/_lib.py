@@ -25,7 +25,7 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_codebook_info", "leech_codebook_class", "leech_codebook_table",
            "leech_fields_from_points", "leech_expand_layout", "leech_layout_scales",
            "leech_host_decode_layout", "leech_gemv", "leech_gemv_grouped", "leech_decode_blocks",
-           "leech_fp16_gemv_ref", "leech_noweights_ctrl"]
+           "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x"]
 
 
 class LeechError(RuntimeError):
@@ -70,6 +70,7 @@ def _load() -> C.CDLL:
         "leech_decode_blocks": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P]),
         "leech_fp16_gemv_ref": (I, [I64, I64, P, P, P, P]),
         "leech_noweights_ctrl": (I, [C.POINTER(LayoutDesc), P, P, P]),
+        "leech_rotate_x": (I, [I64, I64, P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -219,3 +220,7 @@ def fp16_gemv_ref(M, K, d_W, d_x, d_y, stream=0):
 
 def noweights_ctrl(desc, d_x, d_y, stream=0):
     check(lib.leech_noweights_ctrl(C.byref(desc), d_x, d_y, stream or None))
+
+
+def rotate_x(K, Kpad, d_x, d_signs, d_xr, d_xr32=0, stream=0):
+    check(lib.leech_rotate_x(K, Kpad, d_x, d_signs or None, d_xr, d_xr32 or None, stream or None))

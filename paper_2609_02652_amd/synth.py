@@ -218,6 +218,11 @@ def make_activation(K: int, seed: int, name: str) -> np.ndarray:
     return x
 
 
+def make_signs(K: int, seed: int, name: str) -> np.ndarray:
+    """Uniform ±1 signs (int8, length K) for the activation rotation."""
+    return np.where(rng_for(seed, f"{name}/signs").integers(0, 2, K) == 1, 1, -1).astype(np.int8)
+
+
 # Workload shapes (M, K) of the benchmark configurations.
 CONFIG_SHAPES = {
     "c1_768x1536": [("w", 768, 1536)],

@@ -212,6 +212,17 @@ def test_grouped_gemv_validates_groups_before_launch():
         assert e.value.code == code, (rows, cens, _lib.lib.leech_last_error())
 
 
+def test_rotate_validates_before_launch():
+    fake = 256
+    for K, Kpad, code in ((0, 24, -3), (48, 24, -3), (65536, 65544, -3)):
+        with pytest.raises(P.LeechError) as e:
+            _lib.rotate_x(K, Kpad, fake, fake, fake)
+        assert e.value.code == code
+    with pytest.raises(P.LeechError) as e:
+        _lib.rotate_x(24, 24, 0, 0, fake)
+    assert e.value.code == -1
+
+
 def test_lane_cols_fill_the_gpu():
     from paper_2609_02652_amd._lib import LayoutDesc  # noqa: F401
     cases = {768: 16, 1024: 16, 4096: 4, 8192: 2, 14336: 2, 16384: 1, 17408: 1}
