@@ -218,6 +218,19 @@ def bench_layer(args, torch, P, synth):
         for n, w in fp_r[i % fp_reps].items():
             P.fp16_gemv(w, xfor(parts[n]), ys[n])
 
+    # rotated arm: every fused site first rotates its activation (§2.3, §6;
+    # one rotation per site, shared by the site's groups), then runs its GEMV
+    sites = [(f, parts[dict(FUSED_8B)[f][0]]) for f, _ in FUSED_8B]
+    raw = {f: xfor(inp)[:inp.K] for f, inp in sites}
+    signs = {f: torch.from_numpy(synth.make_signs(inp.K, seed=2, name=f"layer8b-{f}")).to(dev)
+             for f, inp in sites}
+    xrot = {f: torch.empty(inp.Kpad, dtype=torch.float16, device=dev) for f, inp in sites}
+
+    def run_fused_rot(i):
+        for f, (m, rows) in fus_r[i % reps].items():
+            P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
+            m.gemv_grouped(xrot[f], rows, [cen] * len(rows), yf[f])
+
     # outputs agree (fused rows are the separate rows, within f32 rounding)
     run_sep(0)
     run_fused(0)
@@ -226,7 +239,7 @@ def bench_layer(args, torch, P, synth):
     rel = float(((yf["qkv"] - ysep).abs().max() / ysep.abs().max()).item())
     res = {}
     for name, fn, nrep in (("separate", run_sep, reps), ("fused", run_fused, reps),
-                           ("fp16", run_fp, fp_reps)):
+                           ("fused_rot", run_fused_rot, reps), ("fp16", run_fp, fp_reps)):
         steps = args.layer_steps
         g = torch.cuda.CUDAGraph()
         fn(0)
@@ -251,11 +264,48 @@ def bench_layer(args, torch, P, synth):
     return {"workload": "one 8B-class decoder layer at batch 1 (q, o 4096x4104; k, v 1024x4104; "
                         "gate, up 14336x4104; down 4096x14352), Planes14",
             "served_bytes": layer_bytes, "us_separate_7_launches": res["separate"],
-            "us_fused_4_launches": res["fused"], "us_fp16_7_launches": res["fp16"],
+            "us_fused_4_launches": res["fused"],
+            "us_fused_with_rotation_8_launches": res["fused_rot"],
+            "us_fp16_7_launches": res["fp16"],
             "fusion_saves": round(1 - res["fused"] / res["separate"], 4),
             "fused_vs_fp16": round(res["fp16"] / res["fused"], 3),
             "fused_GBps": round(layer_bytes / (res["fused"] * 1e-6) / 1e9, 1),
             "qkv_fused_vs_separate_max_rel_diff": rel}
+
+
+def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
+    """µs per activation rotation (blockwise Walsh–Hadamard, fp16 in and out)
+    at the 8B and 14B site widths: one graph replay of args.layer_steps
+    launches, median of three replays (the launch gap included)."""
+    dev = torch.device("cuda:0")
+    res = {}
+    for K in widths:
+        x = torch.from_numpy(synth.make_activation(K, seed=3, name=f"rot{K}")[:K].copy()).to(dev)
+        sg = torch.from_numpy(synth.make_signs(K, seed=3, name=f"rot{K}")).to(dev)
+        Kpad = synth.padded_k(K)
+        out = torch.empty(Kpad, dtype=torch.float16, device=dev)
+        P.rotate_x(x, sg, Kpad, out=out)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(args.layer_steps):
+                P.rotate_x(x, sg, Kpad, out=out)
+        g.replay()
+        torch.cuda.synchronize()
+        meds = []
+        for _ in range(3):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            meds.append(e0.elapsed_time(e1) * 1e3 / args.layer_steps)
+        n = K & -K
+        res[f"K{K}"] = {"us": round(statistics.median(meds), 3), "block": n, "workgroups": K // n}
+        log(f"[bench] rotation K={K}: {res[f'K{K}']}")
+        del g
+    return res
 
 
 def measured_traffic(config):
@@ -368,6 +418,7 @@ def main():
             a._graphs.clear()
         torch.cuda.synchronize()
         layer = bench_layer(args, torch, P, synth)
+        layer["rotation"] = bench_rotation(args, torch, P, synth)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -31,17 +31,39 @@ def pow2_block(K: int) -> int:
     return K & -K
 
 
-def walsh_matrix(n: int) -> np.ndarray:
-    """H_n[i, j] = (−1)^popcount(i & j), as f64 (the textbook definition)."""
-    if n <= 0 or n & (n - 1):
-        raise ValueError("n must be a power of two")
-    i = np.arange(n, dtype=np.int64)
-    parity = np.zeros((n, n), dtype=np.int64)
-    ij = i[:, None] & i[None, :]
-    while ij.any():                       # popcount parity, bit by bit
-        parity ^= ij & 1
-        ij >>= 1
+def _parity16() -> np.ndarray:
+    """popcount(v) mod 2 for v = 0..65535, bit by bit."""
+    v = np.arange(1 << 16, dtype=np.int64)
+    p = np.zeros_like(v)
+    while v.any():
+        p ^= v & 1
+        v >>= 1
+    return p
+
+
+_PARITY16 = _parity16()
+
+
+def walsh_at(n: int, rows) -> np.ndarray:
+    """The given rows of H_n: H_n[i, j] = (−1)^popcount(i & j), as f64 (the
+    textbook definition; the parity of i & j is read 16 bits at a time)."""
+    if n <= 0 or n & (n - 1) or n > 1 << 32:
+        raise ValueError("n must be a power of two ≤ 2^32")
+    i = np.asarray(rows, dtype=np.int64)
+    j = np.arange(n, dtype=np.int64)
+    ij = i[:, None] & j[None, :]
+    parity = _PARITY16[ij & 0xFFFF] ^ _PARITY16[ij >> 16]
     return np.where(parity == 1, -1.0, 1.0)
+
+
+def walsh_rows(n: int, r0: int, r1: int) -> np.ndarray:
+    """Rows r0..r1-1 of H_n."""
+    return walsh_at(n, np.arange(r0, r1))
+
+
+def walsh_matrix(n: int) -> np.ndarray:
+    """H_n, all n rows."""
+    return walsh_rows(n, 0, n)
 
 
 def rotate64(x, signs) -> np.ndarray:
@@ -53,9 +75,32 @@ def rotate64(x, signs) -> np.ndarray:
     if s.size != K or not np.all(np.abs(s) == 1.0):
         raise ValueError("signs must be ±1 of the activation's length")
     n = pow2_block(K)
-    H = walsh_matrix(n)
     blocks = (s * x).reshape(K // n, n)
-    return (blocks @ H.T / np.sqrt(n)).reshape(K)
+    out = np.empty((K // n, n))
+    step = max(1, (1 << 22) // n)          # rows of H_n per piece (bounded memory)
+    for r0 in range(0, n, step):
+        r1 = min(n, r0 + step)
+        out[:, r0:r1] = blocks @ walsh_rows(n, r0, r1).T
+    return (out / np.sqrt(n)).reshape(K)
+
+
+def rotate64_at(x, signs, idx) -> np.ndarray:
+    """Entries idx of rotate64(x, signs), each from its own row of H_n (for
+    checking sampled outputs of long blocks)."""
+    x = np.asarray(x, dtype=np.float64)
+    s = np.asarray(signs, dtype=np.float64)
+    K = x.size
+    if s.size != K or not np.all(np.abs(s) == 1.0):
+        raise ValueError("signs must be ±1 of the activation's length")
+    n = pow2_block(K)
+    idx = np.asarray(idx, dtype=np.int64)
+    sx = s * x
+    out = np.empty(idx.size)
+    for b in np.unique(idx // n):
+        sel = idx // n == b
+        H = walsh_at(n, idx[sel] % n)
+        out[sel] = H @ sx[b * n:(b + 1) * n]
+    return out / np.sqrt(n)
 
 
 def rotate_padded64(x, signs, Kpad: int) -> np.ndarray:

@@ -16,7 +16,7 @@ from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, 
 
 __all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
            "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
-           "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl"]
+           "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x"]
 
 
 def _torch():
@@ -142,10 +142,11 @@ def noweights_ctrl(desc: LayoutDesc, x, y=None, stream=None):
     return y
 
 
-def rotate_x(x, signs=None, Kpad=None, with_f32=False, stream=None):
+def rotate_x(x, signs=None, Kpad=None, with_f32=False, out=None, stream=None):
     """Blockwise Walsh–Hadamard rotation of an fp16 activation (§2.3, §6):
     x fp16 [K], signs int8 ±1 [K] (None: all +1) -> fp16 [Kpad] (zero past K),
-    and the f32 values before rounding when with_f32."""
+    and the f32 values before rounding when with_f32.  `out` (fp16 [Kpad],
+    contiguous) receives the result in place of a new tensor."""
     torch = _torch()
     if x.dtype != torch.float16 or x.dim() != 1 or not x.is_contiguous():
         raise ValueError("x must be a contiguous 1-D fp16 tensor")
@@ -154,7 +155,13 @@ def rotate_x(x, signs=None, Kpad=None, with_f32=False, stream=None):
     if signs is not None and (signs.dtype != torch.int8 or signs.numel() != K
                               or not signs.is_contiguous()):
         raise ValueError("signs must be a contiguous int8 tensor of length K")
-    xr = torch.empty(Kpad, dtype=torch.float16, device=x.device)
+    if out is None:
+        xr = torch.empty(Kpad, dtype=torch.float16, device=x.device)
+    else:
+        if (out.dtype != torch.float16 or out.dim() != 1 or out.numel() != Kpad
+                or not out.is_contiguous() or out.device != x.device):
+            raise ValueError("out must be a contiguous fp16 tensor of length Kpad on x's device")
+        xr = out
     xr32 = torch.empty(K, dtype=torch.float32, device=x.device) if with_f32 else None
     _lib.rotate_x(K, Kpad, x.data_ptr(), signs.data_ptr() if signs is not None else 0,
                   xr.data_ptr(), xr32.data_ptr() if with_f32 else 0, _stream(stream))

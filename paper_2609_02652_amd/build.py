@@ -14,7 +14,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libleech.so")
-SOURCES = [os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "kernels.hip")]
+SOURCES = [os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "kernels.hip"),
+           os.path.join(CSRC, "rotate.hip")]
 ARCH = os.environ.get("LEECH_OFFLOAD_ARCH", "gfx950")
 
 

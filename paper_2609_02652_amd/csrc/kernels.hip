@@ -853,77 +853,6 @@ __global__ __launch_bounds__(512) void fp16_gemv_kernel(const uint16_t* __restri
   if (lane == 0) y[row] = acc;
 }
 
-// ------------------------------------------------------ activation rotation
-// Blockwise Walsh–Hadamard rotation of the activation (§2.3, §6): for K = n·m
-// with n = 2^k the largest power of two dividing K, block b of n coordinates
-// becomes n^(-1/2) · H_n · (s ⊙ x) with H_n[i][j] = (−1)^popcount(i & j).
-// One workgroup per block; the block sits in LDS as f32, one padding word per
-// 16 keeps the radix-16 passes free of bank conflicts.  Each pass transforms
-// up to four index bits: a thread gathers the 16 elements that differ only in
-// those bits, applies the butterflies in registers and scatters them back;
-// butterflies over distinct bits commute, so the passes may take the bits in
-// any order.  Output: binary16 (round to nearest even), zero past K, and
-// optionally the f32 values before that rounding.
-constexpr int kRotThreads = 256;
-constexpr int kRotMaxLog = 15;          // blocks of up to 32768 coordinates
-
-__device__ __forceinline__ int rot_pad(int i) { return i + (i >> 4); }
-
-__global__ __launch_bounds__(kRotThreads) void rotate_kernel(const uint16_t* __restrict__ x,
-                                                             const int8_t* __restrict__ signs,
-                                                             int64_t K, int64_t Kpad, int k,
-                                                             float norm, uint16_t* __restrict__ out,
-                                                             float* __restrict__ out32) {
-  extern __shared__ __attribute__((aligned(16))) float buf[];
-  const int n = 1 << k, tid = threadIdx.x;
-  const int64_t base = (int64_t)blockIdx.x * n;
-  for (int i = tid; i < n; i += kRotThreads) {
-    float v = (float)as_half(x[base + i]);
-    if (signs && signs[base + i] < 0) v = -v;
-    buf[rot_pad(i)] = v;
-  }
-  __syncthreads();
-  for (int lo = 0; lo < k; lo += 4) {
-    const int bits = min(4, k - lo), E = 1 << bits;
-    for (int grp = tid; grp < (n >> bits); grp += kRotThreads) {
-      // index with the pass's bits cleared: the low `lo` bits of grp stay,
-      // the rest move up by `bits`
-      const int b0 = ((grp >> lo) << (lo + bits)) | (grp & ((1 << lo) - 1));
-      float v[16];
-#pragma unroll
-      for (int t = 0; t < 16; ++t)
-        if (t < E) v[t] = buf[rot_pad(b0 + (t << lo))];
-#pragma unroll
-      for (int st = 1; st < 16; st <<= 1) {
-        if (st < E) {
-#pragma unroll
-          for (int t = 0; t < 16; ++t)
-            if (t < E && !(t & st)) {
-              const float a = v[t], b = v[t | st];
-              v[t] = a + b;
-              v[t | st] = a - b;
-            }
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < 16; ++t)
-        if (t < E) buf[rot_pad(b0 + (t << lo))] = v[t];
-    }
-    __syncthreads();
-  }
-  for (int i = tid; i < n; i += kRotThreads) {
-    float v = buf[rot_pad(i)] * norm;
-    // the product is rounded to f32 and then to binary16: the empty asm keeps
-    // the compiler from fusing the scaling and the narrowing into one
-    // mixed-precision multiply that would round only once
-    asm("" : "+v"(v));
-    out[base + i] = __builtin_bit_cast(uint16_t, (_Float16)v);
-    if (out32) out32[base + i] = v;
-  }
-  if (blockIdx.x == gridDim.x - 1)
-    for (int64_t i = K + tid; i < Kpad; i += kRotThreads) out[i] = 0;
-}
-
 // ------------------------------------------------------------- launching
 static int hip_fail(const char* what, hipError_t e) {
   return set_error(LEECH_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -1162,33 +1091,6 @@ int leech_fp16_gemv_ref(int64_t M, int64_t K, const uint16_t* d_W, const uint16_
                      shmem, (hipStream_t)stream, d_W, d_x, d_y, M, K);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("fp16 gemv launch", e);
-  return LEECH_OK;
-}
-
-int leech_rotate_x(int64_t K, int64_t Kpad, const uint16_t* d_x, const int8_t* d_signs,
-                   uint16_t* d_xr, float* d_xr32, void* stream) {
-  clear_error();
-  if (!d_x || !d_xr) return set_error(LEECH_E_ARG, "NULL argument");
-  if (K <= 0 || Kpad < K) return set_error(LEECH_E_SHAPE, "need 0 < K <= Kpad");
-  const int64_t n = K & -K;
-  int k = 0;
-  while ((int64_t)1 << k < n) ++k;
-  if (k > kRotMaxLog)
-    return set_error(LEECH_E_SHAPE, "power-of-two factor of K above 32768 is not supported");
-  if (((uintptr_t)d_x & 1) || ((uintptr_t)d_xr & 1) || ((uintptr_t)d_xr32 & 3))
-    return set_error(LEECH_E_ARG, "misaligned device pointer");
-  // 2^(-k/2): exact for even k, rounded to f32 for odd k
-  const float norm = (float)(1.0 / std::sqrt((double)n));
-  const size_t shmem = (size_t)(n + n / 16) * sizeof(float);
-  if (shmem > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)rotate_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
-    if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
-  }
-  hipLaunchKernelGGL(rotate_kernel, dim3((unsigned)(K / n)), dim3(kRotThreads), shmem,
-                     (hipStream_t)stream, d_x, d_signs, K, Kpad, k, norm, d_xr, d_xr32);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail("rotate launch", e);
   return LEECH_OK;
 }
 

@@ -28,28 +28,59 @@ def dev():
     return torch.device("cuda:0")
 
 
-@pytest.mark.parametrize("K", [24, 1000, 4096, 5120, 14336, 17408, 32768])
-def test_rotation_matches_oracle(dev, K):
-    say(f"[rotate] K={K}")
+def check_rotation(dev, K, Kpad, offset=0):
+    """Rotate through the C ABI and compare with the oracle.  offset > 0 hands
+    the kernel x, signs and both outputs as views `offset` elements into larger
+    buffers, so no pointer is 16-byte aligned (the element-wise path)."""
+    say(f"[rotate] K={K} Kpad={Kpad} offset={offset}")
     x = synth.make_activation(K, seed=K, name="rot")[:K]
     s = synth.make_signs(K, seed=K, name="rot")
-    Kpad = synth.padded_k(K)
-    xr16, xr32 = P.rotate_x(torch.from_numpy(x).to(dev), torch.from_numpy(s).to(dev), Kpad,
-                            with_f32=True)
+    xt = torch.zeros(K + offset, dtype=torch.float16, device=dev)
+    st = torch.ones(K + offset, dtype=torch.int8, device=dev)
+    xt[offset:] = torch.from_numpy(x).to(dev)
+    st[offset:] = torch.from_numpy(s).to(dev)
+    o16 = torch.full((Kpad + offset,), 7.0, dtype=torch.float16, device=dev)[offset:]
+    o32 = torch.empty(K + offset, dtype=torch.float32, device=dev)[offset:]
+    P._lib.rotate_x(K, Kpad, xt[offset:].data_ptr(), st[offset:].data_ptr(), o16.data_ptr(),
+                    o32.data_ptr())
     torch.cuda.synchronize()
-    y16 = xr16.cpu().numpy()
-    y32 = xr32.cpu().numpy().astype(np.float64)
-    y64 = R.rotate64(x, s)
-    k = int(math.log2(R.pow2_block(K)))
+    y16 = o16.cpu().numpy()
+    y32 = o32.cpu().numpy().astype(np.float64)
+    n = R.pow2_block(K)
+    k = int(math.log2(n))
     # f32 butterflies: k stages, each error ≤ 2^-24 · |partial| ≤ 2^-24 · 2^t · max|x|,
     # reaching every output through 2^(k-t) paths; then one rounding of the scale
     bound = (k * 2 ** (k / 2) + 1) * 2.0 ** -24 * np.max(np.abs(x.astype(np.float64)))
-    err = np.max(np.abs(y32 - y64))
-    say(f"    max |f32 - f64| = {err:.3e} (bound {bound:.3e})")
+    if n <= 4096:
+        idx = np.arange(K)
+        y64 = R.rotate64(x, s)
+    else:       # long blocks: 1024 sampled outputs, each from its own row of H_n
+        idx = np.sort(np.random.default_rng(K).choice(K, 1024, replace=False))
+        y64 = R.rotate64_at(x, s, idx)
+    err = np.max(np.abs(y32[idx] - y64))
+    say(f"    max |f32 - f64| = {err:.3e} over {idx.size} outputs (bound {bound:.3e})")
     assert err <= bound
+    # every output: the rotation is orthogonal, so the norm is kept
+    xn = np.linalg.norm(x.astype(np.float64))
+    assert abs(np.linalg.norm(y32) - xn) <= bound * math.sqrt(K)
     # the binary16 output is the f32 value rounded to nearest even, zero past K
     assert np.array_equal(y16[:K].view(np.uint16), y32.astype(np.float32).astype(np.float16).view(np.uint16))
     assert np.all(y16[K:] == 0)
+
+
+# block lengths 2^0 .. 2^15: K = 1, 6, 12 take the blocks shorter than one
+# thread's eight coordinates; 24576 and 49152 the 8192- and 16384-point blocks
+ROT_KS = [1, 6, 12, 24, 44, 1000, 4096, 5120, 14336, 17408, 24576, 49152, 32768]
+
+
+@pytest.mark.parametrize("K", ROT_KS)
+def test_rotation_matches_oracle(dev, K):
+    check_rotation(dev, K, synth.padded_k(K))
+
+
+@pytest.mark.parametrize("K,Kpad", [(7, 13), (4096, 4101), (14336, 14343), (5120, 5120)])
+def test_rotation_unaligned_and_odd_padding(dev, K, Kpad):
+    check_rotation(dev, K, Kpad, offset=1)
 
 
 def test_rotation_without_signs_is_plain_walsh(dev):

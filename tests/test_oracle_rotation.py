@@ -9,7 +9,7 @@ from oracle import rotation as R
 from paper_2609_02652_amd import synth
 
 
-@pytest.mark.parametrize("n", [1, 2, 4, 8, 16, 64, 256, 1024])
+@pytest.mark.parametrize("n", [1, 2, 4, 8, 16, 64, 256, 1024, 4096])
 def test_walsh_matrix_is_sylvester_hadamard(n):
     assert np.array_equal(R.walsh_matrix(n), hadamard(n).astype(np.float64))
 
@@ -69,3 +69,13 @@ def test_planted_natural_order_is_caught():
     rev = [int(f"{i:03b}"[::-1], 2) for i in range(n)]
     wrong = R.walsh_matrix(n)[rev]
     assert not np.array_equal(wrong, hadamard(n))
+
+
+def test_sampled_rows_match_full_rotation():
+    """rotate64_at picks single rows of H_n: it equals rotate64 at those indices
+    (blockwise, across several blocks)."""
+    K = 3 * 256
+    x = np.random.default_rng(11).standard_normal(K)
+    s = np.where(np.random.default_rng(12).integers(0, 2, K) == 1, 1.0, -1.0)
+    idx = np.array([0, 1, 255, 256, 300, 511, 512, 767])
+    assert np.allclose(R.rotate64_at(x, s, idx), R.rotate64(x, s)[idx], rtol=0, atol=1e-12)
