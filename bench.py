@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--no-layer", action="store_true",
                     help="skip the 8B-layer comparison (separate vs fused launches vs FP16)")
     ap.add_argument("--layer-steps", type=int, default=300)
+    ap.add_argument("--no-step14b", action="store_true",
+                    help="skip the 14B-class decode step (40 layers + fp16 head, Leech vs FP16)")
+    ap.add_argument("--step14b-layers", type=int, default=40)
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -273,6 +276,150 @@ def bench_layer(args, torch, P, synth):
             "qkv_fused_vs_separate_max_rel_diff": rel}
 
 
+# One 14B-class decoder layer: hidden 5120, 40 query heads and 8 KV heads of
+# dimension 128, FFN 17408; and the fp16 output head (vocabulary 152064).
+MODEL_14B = [("q", 5120, 5120), ("k", 1024, 5120), ("v", 1024, 5120), ("o", 5120, 5120),
+             ("gate", 17408, 5120), ("up", 17408, 5120), ("down", 5120, 17408)]
+HEAD_14B = (152064, 5120)
+
+
+def replay_us(torch, fn, reps):
+    """µs per call of fn(i), i = 0..reps-1, captured once in a HIP graph:
+    median of three timed replays after one untimed replay."""
+    fn(0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(reps):
+            fn(i)
+    g.replay()
+    torch.cuda.synchronize()
+    meds = []
+    for _ in range(3):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        meds.append(e0.elapsed_time(e1) * 1e3 / reps)
+    del g
+    return statistics.median(meds)
+
+
+def bench_step14b(args, torch, P, synth):
+    """One batch-1 decode step of a 14B-class model through its projections
+    (§3.1's "one token through the projections", at 14B shapes): 40 layers of
+    seven Leech-coded GEMVs each, then the fp16 output head, which is the same
+    in every arm.  Arms: Planes14 in 280 launches; Planes14 fused (q/k/v and
+    gate/up row-concatenated, 160 launches); the fused arm behind the
+    activation rotation of each of the four sites (160 more launches); and FP16
+    weights in 280 launches.  One layer's codes are drawn and every layer
+    holds its own copy in distinct buffers (8.8 GB of Leech bytes, 28 GB of
+    FP16), so every step streams from HBM."""
+    import numpy as np
+    L = args.step14b_layers
+    dev = torch.device("cuda:0")
+    cb = P.Codebook(12)
+    dcb = P.DeviceCodebook(cb, dev)
+    t0 = time.time()
+    parts = {name: synth.make_gemv_inputs(M, K, seed=2000 + i, name=f"step14b-{name}")
+             for i, (name, M, K) in enumerate(MODEL_14B)}
+    log(f"[bench] 14B layer inputs ready in {time.time() - t0:.1f}s")
+    xs = {K: torch.from_numpy(synth.make_activation(K, seed=4, name=f"step14b-x{K}")).to(dev)
+          for K in {K for _, _, K in MODEL_14B}}
+    cen = (1.0, 1.0)
+
+    def leech(names):
+        z = np.concatenate([parts[n].z for n in names])
+        gain = np.concatenate([parts[n].gain for n in names])
+        scale = np.concatenate([parts[n].scale for n in names])
+        cls, sm, lv = cb.fields_from_points(z)
+        return P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, gain, sm, lv, scale, dev)
+
+    def clone(m):
+        return P.LeechMatrix(m.desc, m.main.clone(), m.side0.clone(), m.side1.clone(),
+                             m.scale.clone(), dcb)
+
+    sep0 = {n: leech([n]) for n, _, _ in MODEL_14B}
+    fus0 = {f: (leech(ns), [parts[n].M for n in ns]) for f, ns in FUSED_8B}
+    leech_bytes = sum(m.desc.served_bytes for m in sep0.values())
+    sep = [sep0] + [{n: clone(m) for n, m in sep0.items()} for _ in range(L - 1)]
+    fus = [fus0] + [{f: (clone(m), r) for f, (m, r) in fus0.items()} for _ in range(L - 1)]
+    fp0 = {}
+    for n, m in sep0.items():
+        z, _, _ = m.decode()
+        zf = z.float()
+        inp = parts[n]
+        fac = torch.from_numpy(inp.scale.astype("float32")).to(dev) / zf.pow(2).sum(-1).sqrt()
+        fp0[n] = (zf * fac[..., None]).reshape(inp.M, inp.Kpad).half().contiguous()
+        del z, zf
+    fp = [fp0] + [{n: w.clone() for n, w in fp0.items()} for _ in range(L - 1)]
+    fp_bytes = sum(w.numel() * 2 for w in fp0.values())
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+    head = (torch.randn(HEAD_14B, generator=gen, device=dev) * 0.02).half()
+    y_head = torch.empty(HEAD_14B[0], dtype=torch.float32, device=dev)
+    x_head = xs[HEAD_14B[1]][:HEAD_14B[1]]
+    ys = {n: torch.empty(parts[n].M, dtype=torch.float32, device=dev) for n in parts}
+    yf = {f: torch.empty(sum(r), dtype=torch.float32, device=dev) for f, (_, r) in fus0.items()}
+    site_inp = {f: parts[dict(FUSED_8B)[f][0]] for f, _ in FUSED_8B}
+    raw = {f: xs[inp.K][:inp.K] for f, inp in site_inp.items()}
+    signs = {f: torch.from_numpy(synth.make_signs(inp.K, seed=6, name=f"step14b-{f}")).to(dev)
+             for f, inp in site_inp.items()}
+    xrot = {f: torch.empty(inp.Kpad, dtype=torch.float16, device=dev)
+            for f, inp in site_inp.items()}
+    log(f"[bench] 14B step: {L} layers resident, {L * leech_bytes / 1e9:.2f} GB Planes14, "
+        f"{L * fp_bytes / 1e9:.2f} GB FP16, head {head.numel() * 2 / 1e9:.3f} GB")
+
+    def run_head():
+        P.fp16_gemv(head, x_head, y_head)
+
+    def step_sep(_):
+        for layer in sep:
+            for n, m in layer.items():
+                m.gemv(xs[parts[n].K], ys[n], centroids=cen)
+        run_head()
+
+    def step_fused(_):
+        for layer in fus:
+            for f, (m, rows) in layer.items():
+                m.gemv_grouped(xs[site_inp[f].K], rows, [cen] * len(rows), yf[f])
+        run_head()
+
+    def step_fused_rot(_):
+        for layer in fus:
+            for f, (m, rows) in layer.items():
+                P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
+                m.gemv_grouped(xrot[f], rows, [cen] * len(rows), yf[f])
+        run_head()
+
+    def step_fp(_):
+        for layer in fp:
+            for n, w in layer.items():
+                P.fp16_gemv(w, xs[parts[n].K], ys[n])
+        run_head()
+
+    res = {}
+    for name, fn in (("separate", step_sep), ("fused", step_fused), ("fused_rot", step_fused_rot),
+                     ("fp16", step_fp)):
+        res[name] = round(replay_us(torch, fn, 3), 1)
+        log(f"[bench] 14B step {name}: {res[name]} us")
+    head_us = round(replay_us(torch, lambda _: run_head(), 20), 1)
+    leech_fused = res["fused"] - head_us
+    return {"workload": f"14B-class decode step at batch 1: {L} layers x (q, o 5120x5136; k, v "
+                        f"1024x5136; gate, up 17408x5136; down 5120x17424) Planes14, then the fp16 "
+                        f"head 152064x5120 (same in every arm)",
+            "layers": L, "planes14_bytes": L * leech_bytes, "fp16_bytes": L * fp_bytes,
+            "head_bytes": head.numel() * 2,
+            "us_separate_280": res["separate"], "us_fused_160": res["fused"],
+            "us_fused_with_rotation_320": res["fused_rot"], "us_fp16_280": res["fp16"],
+            "us_head": head_us,
+            "fp16_vs_fused": round(res["fp16"] / res["fused"], 3),
+            "fp16_vs_fused_with_rotation": round(res["fp16"] / res["fused_rot"], 3),
+            "leech_part_GBps_fused": round(L * leech_bytes / (leech_fused * 1e-6) / 1e9, 1)}
+
+
 def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
     """µs per activation rotation (blockwise Walsh–Hadamard, fp16 in and out)
     at the 8B and 14B site widths: one graph replay of args.layer_steps
@@ -419,6 +566,12 @@ def main():
         torch.cuda.synchronize()
         layer = bench_layer(args, torch, P, synth)
         layer["rotation"] = bench_rotation(args, torch, P, synth)
+    step14b = None
+    if not args.no_step14b:
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        step14b = bench_step14b(args, torch, P, synth)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -450,6 +603,7 @@ def main():
                      "traffic": measured_traffic(args.config)},
         "arms": table,
         "layer_8b": layer,
+        "step_14b": step14b,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
