@@ -236,11 +236,16 @@ int leech_noweights_ctrl(const leech_layout_desc* desc, const uint16_t* d_x, flo
  * block b of n consecutive coordinates becomes
  *     xr[b·n + i] = n^(-1/2) · Σ_j H_n[i][j] · s[b·n + j] · x[b·n + j],
  * H_n[i][j] = (−1)^popcount(i & j) (Sylvester-ordered Walsh–Hadamard), with s
- * the caller's ±1 signs (int8 [K]; NULL = all +1).  d_x: binary16 [K];
- * d_xr: binary16 [Kpad], the f32 result rounded to nearest even, zero past K,
- * ready as the GEMV's activation; d_xr32: optional f32 [K] copy of the values
- * before that rounding (NULL to skip).  Arithmetic in f32.  LEECH_E_SHAPE if
- * K ≤ 0, Kpad < K or n > 32768. */
+ * the caller's signs (int8 [K]: a negative entry means −1, any other +1;
+ * NULL = all +1).  d_x: binary16 [K]; d_xr: binary16 [Kpad], the f32 result
+ * rounded to nearest even, zero past K, ready as the GEMV's activation;
+ * d_xr32: optional f32 [K] copy of the values before that rounding (NULL to
+ * skip).  All pointers are caller-owned device memory; d_x and d_xr need
+ * 2-byte, d_xr32 4-byte alignment (16-byte alignment of every pointer, and
+ * 8-byte of d_signs, lets the kernel use vector loads and stores).
+ * Arithmetic in f32; asynchronous on `stream`.  LEECH_E_ARG for a NULL d_x or
+ * d_xr or a misaligned pointer; LEECH_E_SHAPE if K ≤ 0, Kpad < K or
+ * n > 32768. */
 int leech_rotate_x(int64_t K, int64_t Kpad, const uint16_t* d_x, const int8_t* d_signs,
                    uint16_t* d_xr, float* d_xr32, void* stream);
 
