@@ -98,8 +98,13 @@ int leech_codebook_class(const leech_codebook* cb, int class_id, int* shell, int
  *       ascending (bit i = coordinate i); the Golay70 layout's rank indexes it.
  *   LEECH_TABLE_DEVICE: the table every GEMV/decode kernel reads: 512 records
  *       of 32 bytes (see LEECH_DEVICE_TABLE_BYTES); pass its device copy as
- *       d_class_table. */
-enum { LEECH_TABLE_CLASS_LEVELS = 0, LEECH_TABLE_CODEWORDS = 1, LEECH_TABLE_DEVICE = 2 };
+ *       d_class_table.
+ *   LEECH_TABLE_INDEX: the format-v1 index table (class offsets and radices,
+ *       the codewords by value and by weight, binomial coefficients), read by
+ *       leech_transcode_planes14 as d_index_table; exists for the ball
+ *       Λ24(12) and smaller balls (N < 2^47). */
+enum { LEECH_TABLE_CLASS_LEVELS = 0, LEECH_TABLE_CODEWORDS = 1, LEECH_TABLE_DEVICE = 2,
+       LEECH_TABLE_INDEX = 3 };
 #define LEECH_TABLE_SLOTS 512
 #define LEECH_DEVICE_TABLE_BYTES (512 * 32)
 int leech_codebook_table(const leech_codebook* cb, int which, const void** host_ptr,
@@ -178,6 +183,42 @@ int leech_host_decode_layout(const leech_codebook* cb, const leech_layout_desc* 
                              const void* main, const void* side0, const void* side1,
                              int8_t* z, uint16_t* class_id, uint8_t* gain_bit);
 
+/* ------------------------------------------- format-v1 block codes (§2.1) */
+/* A block code is a u64 holding the 47-bit direction index of a point of the
+ * ball (bits 0..46) and the gain bit (bit 47); bits 48..63 are zero (2.000
+ * bits per weight on disk).  The index enumerates the classes in id order,
+ * then inside a class, as one mixed-radix number, most significant digit
+ * first: even classes — the support codeword {i : |z_i| ≡ 2 mod 4} (rank
+ * among the codewords of its weight, ascending value), the arrangement of the
+ * support magnitudes, the arrangement of the other magnitudes, the signs of
+ * the nonzero off-support coordinates, the signs of all support coordinates
+ * but the last (whose sign the sum condition fixes); odd classes — the
+ * codeword {i : z_i ≡ 3 mod 4} (rank among all 4096, ascending value) and the
+ * arrangement of all 24 magnitudes (signs forced).  An arrangement is one
+ * digit per level in ascending order: the colex rank of the level's positions
+ * among those the smaller levels left free. */
+#define LEECH_INDEX_BITS 47
+
+/* Codes of n blocks given as decoded fields (host arrays, as for
+ * leech_expand_layout) -> code[n] (host).  Multithreaded.  Every block is
+ * validated as in leech_expand_layout; the first bad block is named in the
+ * error (LEECH_E_FIELD, LEECH_E_NOT_LATTICE). */
+int leech_index_encode(const leech_codebook* cb, int64_t n, const uint16_t* class_id,
+                       const uint8_t* gain_bit, const uint32_t* sign_mask, const uint8_t* level,
+                       uint64_t* code);
+
+/* Decoded fields of n block codes (host, multithreaded): the load-time
+ * transcoder's first half on the CPU (§2.2).  LEECH_E_FIELD names the first
+ * code with bits above 47 set or an index ≥ N. */
+int leech_index_decode(const leech_codebook* cb, int64_t n, const uint64_t* code,
+                       uint16_t* class_id, uint8_t* gain_bit, uint32_t* sign_mask,
+                       uint8_t* level);
+
+/* The Planes14 descriptor of an M × Kpad matrix, without its fields (the
+ * layout's size does not depend on the codes): what leech_expand_layout's
+ * sizing call returns for LEECH_PLANES14. */
+int leech_planes14_desc(int64_t M, int64_t Kpad, leech_layout_desc* desc);
+
 /* --------------------------------------------------------- device calls */
 
 /* Fused dequantize + GEMV (§2.3): y[r] = Σ_j W[r][j] · x[j] with W decoded on
@@ -248,6 +289,20 @@ int leech_noweights_ctrl(const leech_layout_desc* desc, const uint16_t* d_x, flo
  * n > 32768. */
 int leech_rotate_x(int64_t K, int64_t Kpad, const uint16_t* d_x, const int8_t* d_signs,
                    uint16_t* d_xr, float* d_xr32, void* stream);
+
+/* Load-time transcoder on the device (§2.2: each block's index is expanded
+ * once into its decoded-field record): format-v1 codes -> the Planes14 main
+ * stream, bit-identical to leech_expand_layout's.  desc: a Planes14
+ * descriptor (leech_planes14_desc); d_index_table: device copy of
+ * LEECH_TABLE_INDEX; d_code: u64 [M·nb], row-major (r, j); d_main:
+ * desc->main_bytes bytes, every one written (trailing pad included);
+ * d_bad: one u32 on the device, set to the number of codes that are not
+ * format-v1 codes (their records are written as zeros; the caller must treat
+ * the stream as invalid when it is nonzero).  Asynchronous on `stream`.
+ * LEECH_E_LAYOUT if desc is not Planes14. */
+int leech_transcode_planes14(const leech_layout_desc* desc, const void* d_index_table,
+                             const uint64_t* d_code, void* d_main, uint32_t* d_bad,
+                             void* stream);
 
 #ifdef __cplusplus
 }

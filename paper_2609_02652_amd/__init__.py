@@ -12,11 +12,13 @@ import numpy as np
 
 from . import _lib
 from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, Codebook,
-                   LayoutDesc, LeechError, expand_layout, host_decode_layout, layout_scales)
+                   LayoutDesc, LeechError, expand_layout, host_decode_layout, index_decode,
+                   index_encode, layout_scales, planes14_desc)
 
 __all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
            "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
-           "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x"]
+           "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x",
+           "index_encode", "index_decode", "planes14_desc"]
 
 
 def _torch():
@@ -38,12 +40,14 @@ def _dev(arr: np.ndarray, device):
 
 
 class DeviceCodebook:
-    """Device copies of the class table and the Golay codeword table."""
+    """Device copies of the class table, the Golay codeword table and the
+    format-v1 index table."""
 
     def __init__(self, cb: Codebook, device="cuda"):
         self.cb = cb
         self.table = _dev(cb.table(_lib.TABLE_DEVICE), device)
         self.codewords = _dev(cb.table(_lib.TABLE_CODEWORDS), device)
+        self.index = _dev(cb.table(_lib.TABLE_INDEX), device)
 
 
 class LeechMatrix:
@@ -62,6 +66,28 @@ class LeechMatrix:
         empty = torch.empty(0, dtype=torch.uint8, device=device)
         return cls(desc, _dev(main, device), _dev(s0, device) if s0.size else empty,
                    _dev(s1, device) if s1.size else empty, _dev(sc, device), dcb)
+
+    @classmethod
+    def from_codes(cls, dcb: DeviceCodebook, codes, scale_rowmajor, stream=None):
+        """Planes14 matrix from format-v1 block codes, transcoded on the device
+        (§2.2): codes is an int64 device tensor [M, nb] holding the u64 codes;
+        scale_rowmajor the fp16 block scales [M, nb] (host)."""
+        torch = _torch()
+        if codes.dtype != torch.int64 or codes.dim() != 2 or not codes.is_contiguous():
+            raise ValueError("codes must be a contiguous int64 tensor [M, nb]")
+        M, nb = codes.shape
+        desc = planes14_desc(M, nb * 24)
+        dev = codes.device
+        main = torch.empty(desc.main_bytes, dtype=torch.uint8, device=dev)
+        bad = torch.empty(1, dtype=torch.int32, device=dev)
+        _lib.transcode_planes14(desc, dcb.index.data_ptr(), codes.data_ptr(), main.data_ptr(),
+                                bad.data_ptr(), _stream(stream))
+        n_bad = int(bad.item())
+        if n_bad:
+            raise LeechError(-4, f"{n_bad} of {M * nb} block codes are not format-v1 codes")
+        sc = layout_scales(desc, scale_rowmajor)
+        empty = torch.empty(0, dtype=torch.uint8, device=dev)
+        return cls(desc, main, empty, empty, _dev(sc, dev), dcb)
 
     @property
     def M(self):

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libleech.so")
 SLOT32, PLANES14, PLANES12X, GOLAY70 = 0, 1, 2, 3
 LAYOUTS = {"slot32": SLOT32, "planes14": PLANES14, "planes12x": PLANES12X, "golay70": GOLAY70}
 LAYOUT_NAMES = {v: k for k, v in LAYOUTS.items()}
-TABLE_CLASS_LEVELS, TABLE_CODEWORDS, TABLE_DEVICE = 0, 1, 2
+TABLE_CLASS_LEVELS, TABLE_CODEWORDS, TABLE_DEVICE, TABLE_INDEX = 0, 1, 2, 3
+INDEX_BITS = 47
 ERRORS = {0: "OK", -1: "LEECH_E_ARG", -2: "LEECH_E_LAYOUT", -3: "LEECH_E_SHAPE",
           -4: "LEECH_E_FIELD", -5: "LEECH_E_NOT_LATTICE", -6: "LEECH_E_HIP",
           -7: "LEECH_E_CAPACITY"}
@@ -25,7 +26,9 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_codebook_info", "leech_codebook_class", "leech_codebook_table",
            "leech_fields_from_points", "leech_expand_layout", "leech_layout_scales",
            "leech_host_decode_layout", "leech_gemv", "leech_gemv_grouped", "leech_decode_blocks",
-           "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x"]
+           "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
+           "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
+           "leech_transcode_planes14"]
 
 
 class LeechError(RuntimeError):
@@ -71,6 +74,10 @@ def _load() -> C.CDLL:
         "leech_fp16_gemv_ref": (I, [I64, I64, P, P, P, P]),
         "leech_noweights_ctrl": (I, [C.POINTER(LayoutDesc), P, P, P]),
         "leech_rotate_x": (I, [I64, I64, P, P, P, P, P]),
+        "leech_index_encode": (I, [P, I64, P, P, P, P, P]),
+        "leech_index_decode": (I, [P, I64, P, P, P, P, P]),
+        "leech_planes14_desc": (I, [I64, I64, C.POINTER(LayoutDesc)]),
+        "leech_transcode_planes14": (I, [C.POINTER(LayoutDesc), P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -142,6 +149,41 @@ class Codebook:
         lv = np.empty((n, 24), np.uint8)
         check(lib.leech_fields_from_points(self._h, n, _ptr(z), _ptr(cls), _ptr(sm), _ptr(lv)))
         return cls.reshape(shp), sm.reshape(shp), lv.reshape(shp + (24,))
+
+
+# ----------------------------------------------------- format-v1 block codes
+def index_encode(cb: Codebook, class_id, gain, sign_mask, level) -> np.ndarray:
+    """Decoded fields (any leading shape) -> u64 block codes of that shape."""
+    class_id = np.ascontiguousarray(class_id, np.uint16)
+    shp = class_id.shape
+    n = class_id.size
+    gain = np.ascontiguousarray(gain, np.uint8).reshape(n)
+    sign_mask = np.ascontiguousarray(sign_mask, np.uint32).reshape(n)
+    level = np.ascontiguousarray(level, np.uint8).reshape(n, 24)
+    code = np.empty(n, np.uint64)
+    check(lib.leech_index_encode(cb.handle, n, _ptr(class_id.reshape(n)), _ptr(gain),
+                                 _ptr(sign_mask), _ptr(level), _ptr(code)))
+    return code.reshape(shp)
+
+
+def index_decode(cb: Codebook, code):
+    """u64 block codes -> (class_id, gain, sign_mask, level[..., 24])."""
+    code = np.ascontiguousarray(code, np.uint64)
+    shp = code.shape
+    n = code.size
+    cls = np.empty(n, np.uint16)
+    g = np.empty(n, np.uint8)
+    sm = np.empty(n, np.uint32)
+    lv = np.empty((n, 24), np.uint8)
+    check(lib.leech_index_decode(cb.handle, n, _ptr(code.reshape(n)), _ptr(cls), _ptr(g),
+                                 _ptr(sm), _ptr(lv)))
+    return cls.reshape(shp), g.reshape(shp), sm.reshape(shp), lv.reshape(shp + (24,))
+
+
+def planes14_desc(M: int, Kpad: int) -> LayoutDesc:
+    d = LayoutDesc()
+    check(lib.leech_planes14_desc(M, Kpad, C.byref(d)))
+    return d
 
 
 # ------------------------------------------------------------------- layouts
@@ -224,3 +266,8 @@ def noweights_ctrl(desc, d_x, d_y, stream=0):
 
 def rotate_x(K, Kpad, d_x, d_signs, d_xr, d_xr32=0, stream=0):
     check(lib.leech_rotate_x(K, Kpad, d_x, d_signs or None, d_xr, d_xr32 or None, stream or None))
+
+
+def transcode_planes14(desc, d_index_table, d_code, d_main, d_bad, stream=0):
+    check(lib.leech_transcode_planes14(C.byref(desc), d_index_table, d_code, d_main, d_bad,
+                                       stream or None))

@@ -1,6 +1,6 @@
 """Build libleech.so (HIP for gfx950 + host C++) in place, next to this file.
 
-    python -m paper_2609_02652_amd.build
+    python paper_2609_02652_amd/build.py
 
 Every HIP source is compiled for gfx950 with packed-FP32 instructions
 disabled (-Xclang -target-feature -Xclang -packed-fp32-ops); the host pass of
@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libleech.so")
 SOURCES = [os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "kernels.hip"),
-           os.path.join(CSRC, "rotate.hip")]
+           os.path.join(CSRC, "rotate.hip"), os.path.join(CSRC, "transcode.hip")]
 ARCH = os.environ.get("LEECH_OFFLOAD_ARCH", "gfx950")
 
 
