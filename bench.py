@@ -400,6 +400,8 @@ def bench_step14b(args, torch, P, synth):
                 P.fp16_gemv(w, xs[parts[n].K], ys[n])
         run_head()
 
+    transcode = bench_transcode(torch, P, dcb, parts, dev)
+
     res = {}
     for name, fn in (("separate", step_sep), ("fused", step_fused), ("fused_rot", step_fused_rot),
                      ("fp16", step_fp)):
@@ -417,7 +419,63 @@ def bench_step14b(args, torch, P, synth):
             "us_head": head_us,
             "fp16_vs_fused": round(res["fp16"] / res["fused"], 3),
             "fp16_vs_fused_with_rotation": round(res["fp16"] / res["fused_rot"], 3),
-            "leech_part_GBps_fused": round(L * leech_bytes / (leech_fused * 1e-6) / 1e9, 1)}
+            "leech_part_GBps_fused": round(L * leech_bytes / (leech_fused * 1e-6) / 1e9, 1),
+            "transcode": transcode}
+
+
+BLOCKS_4B = 150_681_600     # blocks of the paper's 4B model (§3.1), for the time to unfold it
+
+
+def bench_transcode(torch, P, dcb, parts, dev):
+    """Load-time unfolding of one 14B layer (§2.2): format-v1 codes -> Planes14
+    streams.  GPU: the transcoder over the seven projections, codes resident
+    in HBM, median of five passes.  Host: the library's multithreaded decode of
+    the codes to fields plus the Planes14 expansion, once."""
+    import numpy as np
+    cb = dcb.cb
+    codes = {}
+    for n, inp in parts.items():
+        cls, sm, lv = cb.fields_from_points(inp.z)
+        codes[n] = P.index_encode(cb, cls, inp.gain, sm, lv)
+    blocks = sum(c.size for c in codes.values())
+    d_codes = {n: torch.from_numpy(c.view(np.int64)).to(dev) for n, c in codes.items()}
+    descs = {n: P.planes14_desc(c.shape[0], c.shape[1] * 24) for n, c in codes.items()}
+    mains = {n: torch.empty(d.main_bytes, dtype=torch.uint8, device=dev) for n, d in descs.items()}
+    bad = torch.zeros(len(codes), dtype=torch.int32, device=dev)
+
+    def run():
+        for i, n in enumerate(codes):
+            P._lib.transcode_planes14(descs[n], dcb.index.data_ptr(), d_codes[n].data_ptr(),
+                                      mains[n].data_ptr(), bad[i:].data_ptr(),
+                                      torch.cuda.current_stream().cuda_stream)
+    run()
+    torch.cuda.synchronize()
+    if int(bad.sum().item()):
+        raise RuntimeError("transcoder rejected valid codes")
+    times = []
+    for _ in range(5):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        run()
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    gpu_us = statistics.median(times)
+    t0 = time.perf_counter()
+    for n, c in codes.items():
+        f = P.index_decode(cb, c)
+        P.expand_layout(cb, P.PLANES14, *f)
+    host_s = time.perf_counter() - t0
+    moved = blocks * (8 + 14)
+    log(f"[bench] transcode {blocks} blocks: GPU {gpu_us:.0f} us, host {host_s:.2f} s")
+    return {"blocks": blocks, "gpu_us": round(gpu_us, 1),
+            "gpu_Mblocks_per_s": round(blocks / gpu_us, 1),
+            "gpu_GBps_codes_in_records_out": round(moved / (gpu_us * 1e-6) / 1e9, 1),
+            "host_s_decode_and_expand": round(host_s, 3), "host_threads": os.cpu_count(),
+            "host_Mblocks_per_s": round(blocks / host_s / 1e6, 2),
+            "gpu_s_for_4B_model_blocks": round(BLOCKS_4B / blocks * gpu_us * 1e-6, 4),
+            "host_s_for_4B_model_blocks": round(BLOCKS_4B / blocks * host_s, 2)}
 
 
 def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
