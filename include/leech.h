@@ -95,16 +95,21 @@ int leech_codebook_class(const leech_codebook* cb, int class_id, int* shell, int
  *       a/(4√m) (round-to-nearest from f64) and a u32 level count, the class
  *       table of §2.3; slots past the last class are zero.
  *   LEECH_TABLE_CODEWORDS: 4096 u32, the extended Golay codewords sorted
- *       ascending (bit i = coordinate i); the Golay70 layout's rank indexes it.
+ *       ascending (bit i = coordinate i).
  *   LEECH_TABLE_DEVICE: the table every GEMV/decode kernel reads: 512 records
  *       of 32 bytes (see LEECH_DEVICE_TABLE_BYTES); pass its device copy as
  *       d_class_table.
+ *   LEECH_TABLE_GOLAY_GEN: 128 u32, the codewords of the 12-bit messages
+ *       a (entries 0..63) and a << 6 (entries 64..127) under the code's
+ *       generator; the codeword of message m is entry (m & 63) XOR entry
+ *       64 + (m >> 6).  The Golay70 layout stores each block's codeword as its
+ *       message; pass this table's device copy as d_codewords.
  *   LEECH_TABLE_INDEX: the format-v1 index table (class offsets and radices,
  *       the codewords by value and by weight, binomial coefficients), read by
  *       leech_transcode_planes14 as d_index_table; exists for the ball
  *       Λ24(12) and smaller balls (N < 2^47). */
 enum { LEECH_TABLE_CLASS_LEVELS = 0, LEECH_TABLE_CODEWORDS = 1, LEECH_TABLE_DEVICE = 2,
-       LEECH_TABLE_INDEX = 3 };
+       LEECH_TABLE_INDEX = 3, LEECH_TABLE_GOLAY_GEN = 4 };
 #define LEECH_TABLE_SLOTS 512
 #define LEECH_DEVICE_TABLE_BYTES (512 * 32)
 int leech_codebook_table(const leech_codebook* cb, int which, const void** host_ptr,
@@ -133,7 +138,7 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *   PLANES12X  two bit planes in a 12-byte record for every block; blocks with
  *              five levels also keep their exact PLANES14 record in an exception
  *              table applied in the same launch (§3.2, sub-4.3 b/w).
- *   GOLAY70    9-byte record: class | gain | 12-bit codeword rank | a 2-bit
+ *   GOLAY70    9-byte record: class | gain | 12-bit codeword message | a 2-bit
  *              in-class code per coordinate; blocks the 2-bit code cannot hold
  *              are exceptions as in PLANES12X (§3.2, 3.6 b/w).
  * Records are stored in "wave tile" order: rows are grouped in tiles of
@@ -224,7 +229,7 @@ int leech_planes14_desc(int64_t M, int64_t Kpad, leech_layout_desc* desc);
 /* Fused dequantize + GEMV (§2.3): y[r] = Σ_j W[r][j] · x[j] with W decoded on
  * the fly from the layout.  d_main/d_side0/d_side1: the layout's streams;
  * d_class_table: device copy of LEECH_TABLE_DEVICE; d_codewords: device copy of
- * LEECH_TABLE_CODEWORDS (GOLAY70 only, else may be NULL); d_scale: fp16 scales
+ * LEECH_TABLE_GOLAY_GEN (GOLAY70 only, else may be NULL); d_scale: fp16 scales
  * in wave-tile order (leech_layout_scales); centroid: the two f32 gain
  * centroids; d_x: binary16 [Kpad]; d_y: f32 [M].  Accumulates in f32; the
  * summation order depends only on (M, Kpad, lane_cols), so every layout of
@@ -249,6 +254,20 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
                        const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
                        const float* group_centroids, const uint16_t* d_x, float* d_y,
                        void* stream);
+
+/* How GOLAY70 GEMVs enqueued from this call on (process-wide) decode the
+ * blocks the 2-bit code cannot hold (§3.2 "Golay70": a plain decoder and one
+ * that hoists work out of the per-slot path).
+ *   LEECH_EXC_HOISTED (default): each workgroup first decodes its tile's
+ *     exception records densely and keeps each one's contribution in LDS; the
+ *     per-block loop then runs the Golay70 decode alone and an exception lane
+ *     takes its kept value.
+ *   LEECH_EXC_INLINE: every wave step that holds an exception decodes it in
+ *     the loop, beside the Golay70 decode of the other lanes.
+ * Both give bit-identical y.  A tile whose exception records exceed the LDS
+ * budget is decoded in line either way.  LEECH_E_ARG for another value. */
+enum { LEECH_EXC_HOISTED = 0, LEECH_EXC_INLINE = 1 };
+int leech_set_exception_mode(int mode);
 
 /* Verification decode on the device with the GEMV's own decoders: z int8
  * [M·nb][24], class_id [M·nb], gain_bit [M·nb], row-major (r, j).  Any output

@@ -13,12 +13,14 @@ import numpy as np
 from . import _lib
 from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, Codebook,
                    LayoutDesc, LeechError, expand_layout, host_decode_layout, index_decode,
-                   index_encode, layout_scales, planes14_desc)
+                   index_encode, layout_scales, planes14_desc, set_exception_mode,
+                   EXC_HOISTED, EXC_INLINE)
 
 __all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
            "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
            "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x",
-           "index_encode", "index_decode", "planes14_desc"]
+           "index_encode", "index_decode", "planes14_desc", "set_exception_mode",
+           "EXC_HOISTED", "EXC_INLINE"]
 
 
 def _torch():
@@ -40,13 +42,14 @@ def _dev(arr: np.ndarray, device):
 
 
 class DeviceCodebook:
-    """Device copies of the class table, the Golay codeword table and the
-    format-v1 index table."""
+    """Device copies of the class table, the Golay codeword and generator
+    tables and the format-v1 index table."""
 
     def __init__(self, cb: Codebook, device="cuda"):
         self.cb = cb
         self.table = _dev(cb.table(_lib.TABLE_DEVICE), device)
         self.codewords = _dev(cb.table(_lib.TABLE_CODEWORDS), device)
+        self.golay_gen = _dev(cb.table(_lib.TABLE_GOLAY_GEN), device)
         self.index = _dev(cb.table(_lib.TABLE_INDEX), device)
 
 
@@ -111,7 +114,7 @@ class LeechMatrix:
         elif y.dtype != torch.float32 or y.numel() != self.M or not y.is_contiguous():
             raise ValueError("y must be a contiguous f32 tensor of length M")
         m, s0, s1 = self._ptrs()
-        _lib.gemv(self.desc, m, s0, s1, self.dcb.table.data_ptr(), self.dcb.codewords.data_ptr(),
+        _lib.gemv(self.desc, m, s0, s1, self.dcb.table.data_ptr(), self.dcb.golay_gen.data_ptr(),
                   self.scale.data_ptr(), centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
         return y
 
@@ -128,7 +131,7 @@ class LeechMatrix:
             raise ValueError("y must be a contiguous f32 tensor of length M")
         m, s0, s1 = self._ptrs()
         _lib.gemv_grouped(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
-                          self.dcb.codewords.data_ptr(), self.scale.data_ptr(), group_rows,
+                          self.dcb.golay_gen.data_ptr(), self.scale.data_ptr(), group_rows,
                           group_centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
         return y
 
@@ -142,7 +145,7 @@ class LeechMatrix:
         g = torch.empty((M, nb), dtype=torch.uint8, device=dev)
         m, s0, s1 = self._ptrs()
         _lib.decode_blocks(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
-                           self.dcb.codewords.data_ptr(), z.data_ptr(), c.data_ptr(), g.data_ptr(),
+                           self.dcb.golay_gen.data_ptr(), z.data_ptr(), c.data_ptr(), g.data_ptr(),
                            _stream(stream))
         return z, c, g
 

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libleech.so")
 SLOT32, PLANES14, PLANES12X, GOLAY70 = 0, 1, 2, 3
 LAYOUTS = {"slot32": SLOT32, "planes14": PLANES14, "planes12x": PLANES12X, "golay70": GOLAY70}
 LAYOUT_NAMES = {v: k for k, v in LAYOUTS.items()}
-TABLE_CLASS_LEVELS, TABLE_CODEWORDS, TABLE_DEVICE, TABLE_INDEX = 0, 1, 2, 3
+TABLE_CLASS_LEVELS, TABLE_CODEWORDS, TABLE_DEVICE, TABLE_INDEX, TABLE_GOLAY_GEN = 0, 1, 2, 3, 4
 INDEX_BITS = 47
 ERRORS = {0: "OK", -1: "LEECH_E_ARG", -2: "LEECH_E_LAYOUT", -3: "LEECH_E_SHAPE",
           -4: "LEECH_E_FIELD", -5: "LEECH_E_NOT_LATTICE", -6: "LEECH_E_HIP",
@@ -28,7 +28,7 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_host_decode_layout", "leech_gemv", "leech_gemv_grouped", "leech_decode_blocks",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
-           "leech_transcode_planes14"]
+           "leech_transcode_planes14", "leech_set_exception_mode"]
 
 
 class LeechError(RuntimeError):
@@ -78,6 +78,7 @@ def _load() -> C.CDLL:
         "leech_index_decode": (I, [P, I64, P, P, P, P, P]),
         "leech_planes14_desc": (I, [I64, I64, C.POINTER(LayoutDesc)]),
         "leech_transcode_planes14": (I, [C.POINTER(LayoutDesc), P, P, P, P, P]),
+        "leech_set_exception_mode": (I, [I]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -271,3 +272,11 @@ def rotate_x(K, Kpad, d_x, d_signs, d_xr, d_xr32=0, stream=0):
 def transcode_planes14(desc, d_index_table, d_code, d_main, d_bad, stream=0):
     check(lib.leech_transcode_planes14(C.byref(desc), d_index_table, d_code, d_main, d_bad,
                                        stream or None))
+
+
+EXC_HOISTED, EXC_INLINE = 0, 1
+
+
+def set_exception_mode(mode: int) -> None:
+    """Process-wide: how Golay70 GEMVs enqueued afterwards decode exceptions."""
+    check(lib.leech_set_exception_mode(mode))

@@ -40,6 +40,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstdlib>
@@ -65,6 +66,9 @@ constexpr float kTwo24 = 16777216.0f;
 // so the eight prefetch slots and the exception-path decode stay in registers.
 constexpr int kMaxWaves = 8;
 constexpr int kExcLdsBytes = 32 * 1024;   // a tile's exception records staged in LDS
+// Golay70, hoisted: the f32 contribution (block sum × factor) of each of a
+// tile's exceptions, plus one spare slot
+constexpr int kPreFloats = kExcLdsBytes / kPlanes14Bytes + 2;
 constexpr int kTableBytes = 1024 * 16;    // LDS class-table entries (class | gain << 9)
 // Raw buffer descriptor, word 3, for the gfx9 family (32-bit elements, no
 // swizzle); loads carry the non-temporal hint: records and scales are read once.
@@ -95,6 +99,7 @@ struct GemvArgs {
   int ngroups;
   int64_t grp_end[LEECH_MAX_GROUPS];      // first row past each group
   float grp_cen[LEECH_MAX_GROUPS][2];
+  int inline_exc;               // Golay70: 1 = exceptions decoded in the loop
 };
 
 // Where side data comes from: global memory (verification decode, and the
@@ -162,6 +167,8 @@ struct G70Entry {
   uint32_t alo, ahi;    // |value| at side·4 + code
   uint32_t slo, shi;    // 0x80 where that value is negative
 };
+constexpr int kG70Entries = 304;    // the ball's 301 classes, rounded to 16
+constexpr int kG70LdsBytes = kG70Entries * 16 + 128 * 4;   // entries + generator table
 
 __device__ __forceinline__ uint32_t align(uint32_t hi, uint32_t lo, uint32_t s) {
   return __builtin_amdgcn_alignbit(hi, lo, s);
@@ -266,12 +273,14 @@ struct Lane {
   uint32_t rec;
   uint32_t sh;
   uint32_t esh;
+  bool own;         // the lane holds a block of its own (not a stand-in)
 };
 // u: the unit base's byte offset modulo 4
-__device__ __forceinline__ Lane lane_place(uint32_t ul, uint32_t stride, uint32_t u) {
+__device__ __forceinline__ Lane lane_place(uint32_t ul, uint32_t stride, uint32_t u,
+                                           bool own = true) {
   const uint32_t off = ul * stride + u;
   const uint32_t sh = (off & 3u) * 8u;
-  return Lane{ul, off & ~3u, sh, (sh + 28u) & 31u};
+  return Lane{ul, off & ~3u, sh, (sh + 28u) & 31u, own};
 }
 
 // Words a lane prefetches for one block.
@@ -405,7 +414,7 @@ __device__ __forceinline__ Pref load_unit(const GemvArgs& a, const TileCtx& t, b
       constexpr uint32_t S = Stride<LAYOUT>::v;
       const uint32_t ub = blk * S;
       Lane l = L;
-      if constexpr (!EVEN) l = lane_place(L.ul, S, ub & 3u);
+      if constexpr (!EVEN) l = lane_place(L.ul, S, ub & 3u, L.own);
       const int soff = (int)(ub & ~3u);
       if constexpr (LAYOUT == LEECH_PLANES14) {
         const u32x4a w = __builtin_amdgcn_raw_buffer_load_b128(live ? t.rec : null_rsrc(), (int)l.rec,
@@ -437,9 +446,8 @@ __device__ __forceinline__ LdsEntry make_entry(const DevClass* tab, uint32_t e, 
   return t;
 }
 
-__device__ __forceinline__ G70Entry make_g70(const DevClass* tab, uint32_t c) {
-  const u32x4a d = *(const u32x4a*)&tab[c];
-  const u32x4a v = *((const u32x4a*)&tab[c] + 1);        // g70[8], g70abs[8]
+// G70Entry of a class from the two halves of its 32-byte table record.
+__device__ __forceinline__ G70Entry g70_entry(const u32x4a& d, const u32x4a& v) {
   G70Entry t;
   t.alo = v.z;
   t.ahi = v.w;
@@ -452,6 +460,15 @@ __device__ __forceinline__ G70Entry make_g70(const DevClass* tab, uint32_t c) {
   t.slo = slo;
   t.shi = shi;
   return t;
+}
+
+__device__ __forceinline__ G70Entry make_g70(const DevClass* tab, uint32_t c) {
+  return g70_entry(*(const u32x4a*)&tab[c], *((const u32x4a*)&tab[c] + 1));
+}
+
+// Golay codeword of a 12-bit message from the 128-entry generator table.
+__device__ __forceinline__ uint32_t golay_word(const uint32_t* gen, uint32_t m) {
+  return gen[m & 63u] ^ gen[64u + (m >> 6)];
 }
 
 // x of block j in the cores' pair order: three 16-byte loads, then pair k
@@ -519,13 +536,15 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const int xblocks = groups * C;
   uint32_t* xs = (uint32_t*)smem;                                       // xblocks × 12 x pairs
   uint8_t* p = smem + (size_t)xblocks * 48;
-  G70Entry* gs = (G70Entry*)p;                                          // Golay70: 512 entries
-  uint32_t* cws = (uint32_t*)(p + 512 * sizeof(G70Entry));              // 4096 words
-  if constexpr (LAYOUT == LEECH_GOLAY70) p += 512 * sizeof(G70Entry) + 4096 * 4;
+  G70Entry* gs = (G70Entry*)p;                                          // Golay70: 301 entries
+  uint32_t* cws = (uint32_t*)(p + kG70Entries * sizeof(G70Entry));      // 128 words
+  if constexpr (LAYOUT == LEECH_GOLAY70) p += kG70LdsBytes;
   uint8_t* units_lds = p;                                               // groups × 16 B
   if constexpr (kUnits) p += (size_t)groups * kUnitEntryBytes;
   uint8_t* exc_lds = p;                                                 // ≤ kExcLdsBytes
   if constexpr (kExc) p += kExcLdsBytes;
+  float* pre = (float*)p;                                               // Golay70: kPreFloats
+  if constexpr (LAYOUT == LEECH_GOLAY70) p += kPreFloats * 4;
   float* red = (float*)p;                                               // waves × 64
 
   const int tid = threadIdx.x, nthr = blockDim.x;
@@ -541,8 +560,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // 24-bit products: a 64-bit multiply-add chosen for these would read an
   // undefined high half that may sit in a register with a load in flight, and
   // the wait for it drains every outstanding load
-  const Lane Lf = lane_place(row_ok ? __umul24(rl, C) + cl : 0u, S, 0u);
-  const Lane Ll = lane_place(last_ok ? __umul24(rl, C_last) + cl : 0u, S, 0u);
+  const Lane Lf = lane_place(row_ok ? __umul24(rl, C) + cl : 0u, S, 0u, row_ok);
+  const Lane Ll = lane_place(last_ok ? __umul24(rl, C_last) + cl : 0u, S, 0u, last_ok);
   // the pipeline's lane place and its stand-in unit: a full unit when there is
   // one, else the last (then the pipeline processes nothing)
   const Lane Lp = gf > 0 ? Lf : Ll;
@@ -562,6 +581,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const GlobalSide gside{&a};
   LdsSide side{&a, exc_lds, 0, false, units_lds, tile * groups, 0u};
   uint64_t exc_chunks = 0;
+  uint32_t exc_first = 0, exc_count = 0;    // the tile's exception records
   if constexpr (kExc) {
     uint64_t e0, e1;
     if constexpr (LAYOUT == LEECH_PLANES12X) {
@@ -583,6 +603,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     const uint64_t end = e1 * kPlanes14Bytes + 2;
     exc_chunks = (end - side.exc_start + 15) / 16;
     side.exc_in_lds = exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
+    exc_first = (uint32_t)e0;
+    exc_count = (uint32_t)(e1 - e0);
   }
 
   // Prologue, ordered for the in-order load counter: first the staging loads
@@ -616,11 +638,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     for (int c = tid + nthr; c < kBallClasses; c += nthr) {
       ts[c] = make_entry(a.table, (uint32_t)c, cen0, cen1);
       ts[c + 512] = make_entry(a.table, (uint32_t)c | 512u, cen0, cen1);
+      if constexpr (LAYOUT == LEECH_GOLAY70) gs[c] = make_g70(a.table, (uint32_t)c);
     }
-  if constexpr (LAYOUT == LEECH_GOLAY70) {
-    for (int c = tid; c < 512; c += nthr) gs[c] = make_g70(a.table, (uint32_t)c);
-    for (int k = tid; k < 1024; k += nthr) ((u32x4a*)cws)[k] = ((const u32x4a*)a.codewords)[k];
-  }
   const uint8_t* side_units = LAYOUT == LEECH_SLOT32 ? a.side0 : a.side1;
   if constexpr (kUnits)
     for (int u = tid + kUPer * nthr; u < groups; u += nthr)
@@ -643,11 +662,18 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     xr[q].v1 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
     xr[q].v2 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 32, 0, 0);
   }
-  u32x4a tr = {0, 0, 0, 0};
+  u32x4a tr = {0, 0, 0, 0}, tr2 = {0, 0, 0, 0}, gr = {0, 0, 0, 0};
   if constexpr (kW) {
     const __amdgpu_buffer_rsrc_t r =
         wave * 64 < kBallClasses ? make_rsrc(a.table, kBallClasses * sizeof(DevClass)) : null_rsrc();
     tr = __builtin_amdgcn_raw_buffer_load_b128(r, tid * (int)sizeof(DevClass), 0, 0);
+    if constexpr (LAYOUT == LEECH_GOLAY70) {
+      // the Golay70 value tables (second half of each class record) and the
+      // 128-word generator table (wave 0)
+      tr2 = __builtin_amdgcn_raw_buffer_load_b128(r, tid * (int)sizeof(DevClass) + 16, 0, 0);
+      const __amdgpu_buffer_rsrc_t rg = wave == 0 ? make_rsrc(a.codewords, 512) : null_rsrc();
+      gr = __builtin_amdgcn_raw_buffer_load_b128(rg, tid * 16, 0, 0);
+    }
   }
   u32x4a ur[kUPer], er[kEPer];
   if constexpr (kUnits) {
@@ -690,7 +716,10 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       ts[tid] = e;
       e.factor = f * cen1;
       ts[tid + 512] = e;
+      if constexpr (LAYOUT == LEECH_GOLAY70) gs[tid] = g70_entry(tr, tr2);
     }
+    if constexpr (LAYOUT == LEECH_GOLAY70)
+      if (tid < 32) ((u32x4a*)cws)[tid] = gr;
   }
   if constexpr (kUnits) {
 #pragma unroll
@@ -710,7 +739,51 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     return *(const LdsEntry*)__builtin_assume_aligned((const uint8_t*)ts + e16, 16);
   };
   auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
-  auto cw = [&](uint32_t r) -> uint32_t { return cws[r]; };
+  auto cw = [&](uint32_t m) -> uint32_t { return golay_word(cws, m); };
+
+  // Golay70, hoisted decoder: the tile's exceptions (their exact Planes14
+  // records are in LDS) are decoded once, densely, before the loop, and each
+  // one's contribution dot12 · factor is kept in LDS; the loop then runs the
+  // Golay70 decode alone and a lane holding an exception takes the kept value
+  // in place of its own.  Same products, same order: y is unchanged.
+  bool hoisted = false;
+  if constexpr (LAYOUT == LEECH_GOLAY70) {
+    hoisted = !a.inline_exc && side.exc_in_lds;
+    if (hoisted) {
+      for (uint32_t e = tid; e < exc_count; e += nthr) {
+        const uint32_t ex = exc_first + e;
+        // its unit: the last one whose first exception index is ≤ ex
+        int lo = 0, hi = groups - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          uint64_t b;
+          uint32_t base;
+          side.unit_entry(nullptr, tile * groups + mid, b, base);
+          if (base <= ex) lo = mid;
+          else hi = mid - 1;
+        }
+        uint64_t bits;
+        uint32_t base;
+        side.unit_entry(nullptr, tile * groups + lo, bits, base);
+        for (uint32_t k = ex - base; k; --k) bits &= bits - 1;   // its place in the unit
+        const uint32_t ul = (uint32_t)__builtin_ctzll(bits);
+        const uint32_t cols = lo == gf ? (uint32_t)C_last : (uint32_t)C;
+        const uint32_t* xj = xs + 12 * (lo * C + ul % cols);
+        uint32_t xw[12];
+#pragma unroll
+        for (int k = 0; k < 12; ++k) xw[k] = xj[k];
+        uint32_t w[4], sh, e16, p0, p1, p2, pos, h[12];
+        side.exc_window(ex, w, sh);
+        planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
+        const LdsEntry te = tab(e16);
+        planes_core(p0, p1, p2, pos, te.tlo, te.thi, h);
+        pre[e] = dot12(h, xw) * te.factor;
+      }
+      if (tid == 0) pre[exc_count] = 0.0f;
+      __syncthreads();
+    }
+  }
+
   const uint8_t* x_lane = (const uint8_t*)xs + __umul24(cl, 48u);
   float acc = 0.0f;
   // One unit: decode slot p for unit g and accumulate.
@@ -726,6 +799,27 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       acc += dot12(ones, xw);
     } else {
       uint32_t h[12], e16;
+      if constexpr (LAYOUT == LEECH_GOLAY70) {
+        if (hoisted) {
+          const uint32_t r0 = align(pr.w1, pr.w0, pr.sh), r1 = align(pr.w2, pr.w1, pr.sh);
+          const uint32_t r2 = pr.w2 >> pr.sh;
+          e16 = (r0 << 4) & 0x3FF0u;
+          golay70_core(align(r1, r0, 22), align(r2, r1, 14), cw((r0 >> 10) & 0xFFFu),
+                       g70((e16 >> 4) & 511u), h);
+          float v = dot12(h, xw) * tab(e16).factor;
+          uint64_t bits;
+          uint32_t base;
+          side.unit_entry(nullptr, tile * groups + g, bits, base);
+          const uint32_t ei =
+              base - exc_first + (uint32_t)__builtin_popcountll(bits & ((1ull << L.ul) - 1ull));
+          // a stand-in lane (past the last column) has zero x and must add
+          // zero, not the contribution kept for the block it stands in for
+          const float kept = pre[min(ei, exc_count)];
+          v = ((r2 >> 6) & 1u) && L.own ? kept : v;
+          acc = __builtin_fmaf((float)as_half(pr.scale), v, acc);
+          return;
+        }
+      }
       decode_block<LAYOUT>(pr, L.ul, tile, tile * groups + g, tab, g70, cw, side, a, h, e16);
       const float s = dot12(h, xw);
       acc = __builtin_fmaf((float)as_half(pr.scale), s * tab(e16).factor, acc);
@@ -800,7 +894,7 @@ __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, u
   }
   auto tab = [&](uint32_t e16) -> LdsEntry { return make_entry(a.table, e16 >> 4, 1.0f, 1.0f); };
   auto g70 = [&](uint32_t c) -> G70Entry { return make_g70(a.table, c); };
-  auto cw = [&](uint32_t rk) -> uint32_t { return a.codewords[rk]; };
+  auto cw = [&](uint32_t m) -> uint32_t { return golay_word(a.codewords, m); };
   uint32_t h[12], e16;
   decode_block<LAYOUT>(p, ul, tile, tile * (int)a.groups + g, tab, g70, cw, side, a, h, e16);
   int8_t z[kDim];
@@ -854,6 +948,9 @@ __global__ __launch_bounds__(512) void fp16_gemv_kernel(const uint16_t* __restri
 }
 
 // ------------------------------------------------------------- launching
+// How GEMV launches enqueued from now on decode Golay70 exceptions.
+static std::atomic<int> g_exc_mode{LEECH_EXC_HOISTED};
+
 static int hip_fail(const char* what, hipError_t e) {
   return set_error(LEECH_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
@@ -892,6 +989,7 @@ static GemvArgs make_args(const leech_layout_desc* d) {
   a.R = kWave / d->lane_cols;
   a.groups = (d->nb + a.C - 1) / a.C;
   a.waves = waves_for(a.groups);
+  a.inline_exc = g_exc_mode.load(std::memory_order_relaxed) == LEECH_EXC_INLINE;
   a.tiles = (d->M + a.R - 1) / a.R;
   a.n_exc = d->n_exceptions;
   a.main_bytes = d->main_bytes;
@@ -911,9 +1009,10 @@ static bool even_bases(const GemvArgs& a, int layout) {
 template <int LAYOUT>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
   return (size_t)a.groups * a.C * 48 +
-         (LAYOUT == LEECH_GOLAY70 ? 512 * sizeof(G70Entry) + 4096 * 4 : 0) +
+         (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
-         (has_exc<LAYOUT>() ? kExcLdsBytes : 0) + (size_t)a.waves * 64 * 4;
+         (has_exc<LAYOUT>() ? kExcLdsBytes : 0) +
+         (LAYOUT == LEECH_GOLAY70 ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
 }
 
 template <int LAYOUT, bool EVEN>
@@ -1091,6 +1190,14 @@ int leech_fp16_gemv_ref(int64_t M, int64_t K, const uint16_t* d_W, const uint16_
                      shmem, (hipStream_t)stream, d_W, d_x, d_y, M, K);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("fp16 gemv launch", e);
+  return LEECH_OK;
+}
+
+int leech_set_exception_mode(int mode) {
+  clear_error();
+  if (mode != LEECH_EXC_HOISTED && mode != LEECH_EXC_INLINE)
+    return set_error(LEECH_E_ARG, "exception mode must be LEECH_EXC_HOISTED or LEECH_EXC_INLINE");
+  g_exc_mode.store(mode, std::memory_order_relaxed);
   return LEECH_OK;
 }
 

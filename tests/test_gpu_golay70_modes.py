@@ -1,0 +1,102 @@
+"""Golay70's two exception decoders (hoisted pre-pass, in line) through the C
+ABI: bit-identical y to each other and to Planes14, and to the oracle within
+tolerance, on the usual shapes and on a tile whose exception records exceed the
+LDS budget (decoded from global memory in both modes)."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import paper_2609_02652_amd as P  # noqa: E402
+from paper_2609_02652_amd import synth  # noqa: E402
+from oracle import decode as D  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+CEN = (0.75, 1.25)
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def dcb(dev):
+    return P.DeviceCodebook(P.Codebook(12), dev)
+
+
+def y_in_mode(mat, x, mode):
+    P.set_exception_mode(mode)
+    try:
+        y = mat.gemv(x, centroids=CEN).cpu().numpy()
+    finally:
+        P.set_exception_mode(P.EXC_HOISTED)
+    return y
+
+
+def check(dev, dcb, inp, label):
+    cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+    g70 = P.LeechMatrix.from_fields(dcb, P.GOLAY70, cls, inp.gain, sm, lv, inp.scale, dev)
+    p14 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    say(f"[golay70 modes] {label}: {g70.desc.n_exceptions} exceptions of {inp.M * inp.nb}")
+    x = torch.from_numpy(inp.x).to(dev)
+    yh = y_in_mode(g70, x, P.EXC_HOISTED)
+    yi = y_in_mode(g70, x, P.EXC_INLINE)
+    yp = p14.gemv(x, centroids=CEN).cpu().numpy()
+    assert np.array_equal(yh.view(np.uint32), yi.view(np.uint32)), "modes differ"
+    assert np.array_equal(yh.view(np.uint32), yp.view(np.uint32)), "differs from Planes14"
+    W = D.weights64_from_points(inp.z, inp.gain, inp.scale, CEN)
+    e = D.errors(yh, D.gemv64(W, inp.x), W, inp.x)
+    assert e["max_norm_err"] <= 2e-3 and e["max_abs_err"] <= 1e-5, e
+    return g70
+
+
+@pytest.mark.parametrize("M,K", [(1, 24), (65, 408), (257, 792), (768, 1536), (16385, 120)])
+def test_modes_agree(dev, dcb, M, K):
+    check(dev, dcb, synth.make_gemv_inputs(M, K, seed=M + K, name="g70modes"), f"{M}x{K}")
+
+
+def exception_points(cb, n, seed):
+    """n drawn points that Golay70 cannot hold with its 2-bit code: the host
+    expansion of a one-column matrix flags them (record bit 70), and with one
+    block per row the storage slot of row r is r."""
+    pool = synth.sample_ball_points(synth.rng_for(seed, "g70-exc"), 40 * n)
+    cls, sm, lv = cb.fields_from_points(pool)
+    gain = np.zeros(len(pool), np.uint8)
+    d, main, _, _ = P.expand_layout(cb, P.GOLAY70, cls[:, None], gain[:, None], sm[:, None],
+                                    lv[:, None, :])
+    flags = (main[: 9 * len(pool)].reshape(-1, 9)[:, 8] >> 6) & 1
+    picked = pool[flags == 1]
+    assert len(picked) >= n, "pool too small"
+    return picked[:n]
+
+
+def test_tile_over_the_lds_budget(dev, dcb):
+    """8 × 14400: lane_cols 16, two tiles of 4 rows × 600 blocks.  The first
+    tile holds only exceptions (2400 records, more than the 32 KiB staged in
+    LDS): it is decoded in line from global memory in both modes; the second
+    is an ordinary tile."""
+    M, K = 8, 14400
+    inp = synth.make_gemv_inputs(M, K, seed=31, name="g70-heavy")
+    z = inp.z.copy()
+    z[:4] = exception_points(dcb.cb, 4 * inp.nb, seed=31).reshape(4, inp.nb, 24)
+    inp = synth.GemvInputs(M, inp.K, inp.Kpad, inp.nb, z, inp.gain, inp.scale, inp.x, inp.seed,
+                           inp.name)
+    g70 = check(dev, dcb, inp, "heavy tile")
+    assert g70.desc.n_exceptions >= 4 * inp.nb
+    z_dev, _, _ = g70.decode()
+    assert np.array_equal(z_dev.cpu().numpy(), z)
+
+
+def test_mode_is_validated():
+    with pytest.raises(P.LeechError, match="LEECH_E_ARG"):
+        P.set_exception_mode(7)

@@ -59,6 +59,12 @@ def test_class_level_table_bit_exact(cb):
 def test_codeword_table(cb):
     cw = cb.table(_lib.TABLE_CODEWORDS).view(np.uint32)
     assert list(cw) == list(L.golay_codewords())
+    # the generator table: entry (m & 63) ^ entry 64 + (m >> 6) over all 4096
+    # messages gives every codeword once
+    gen = cb.table(_lib.TABLE_GOLAY_GEN).view(np.uint32)
+    assert gen.size == 128
+    words = sorted(int(gen[m & 63] ^ gen[64 + (m >> 6)]) for m in range(4096))
+    assert words == sorted(L.golay_codewords())
 
 
 def test_fields_match_oracle(cb):
