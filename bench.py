@@ -30,7 +30,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published peak
 REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Cache
-ARMS = ["planes14", "slot32", "planes12x", "golay70", "golay70_inline", "fp16", "noweights"]
+ARMS = ["planes14", "slot32", "planes12x", "planes12x_inline", "golay70", "golay70_inline",
+        "fp16", "noweights"]
 CONFIGS = {"c1_768x1536": (768, 1536), "c2_4096x4096": (4096, 4096),
            "c4_8192x8192": (8192, 8192)}
 
@@ -102,7 +103,7 @@ def build_arms(args, torch, P, synth):
     base_desc = None
     mat14 = None
     for name in ("planes14", "slot32", "planes12x", "golay70"):
-        if name not in wanted and not (name == "planes14"):
+        if name not in wanted and f"{name}_inline" not in wanted and name != "planes14":
             continue
         mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[name], cls, inp.gain, sm, lv, inp.scale, dev)
         served = mat.desc.served_bytes
@@ -113,7 +114,7 @@ def build_arms(args, torch, P, synth):
         arms[name] = Arm(name, [(lambda m=m: m.gemv(x, y)) for m in mats], served, mat.desc)
         if name == "planes14":
             base_desc, mat14 = mat.desc, mat
-        if name == "golay70" and "golay70_inline" in wanted:
+        if name in ("planes12x", "golay70") and f"{name}_inline" in wanted:
             # the plain decoder: exceptions decoded in the loop (the mode is
             # read when a launch is enqueued, so graphs keep it)
             def inline(m):
@@ -122,7 +123,7 @@ def build_arms(args, torch, P, synth):
                     m.gemv(x, y)
                 finally:
                     P.set_exception_mode(P.EXC_HOISTED)
-            arms["golay70_inline"] = Arm("golay70_inline", [(lambda m=m: inline(m)) for m in mats],
+            arms[f"{name}_inline"] = Arm(f"{name}_inline", [(lambda m=m: inline(m)) for m in mats],
                                          served, mat.desc)
         log(f"[bench] {name}: {served} served bytes/GEMV, {reps} replicas")
     if "fp16" in wanted:

@@ -137,7 +137,9 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *              inverted sign mask (bit i set iff z_i ≥ 0).
  *   PLANES12X  two bit planes in a 12-byte record for every block; blocks with
  *              five levels also keep their exact PLANES14 record in an exception
- *              table applied in the same launch (§3.2, sub-4.3 b/w).
+ *              table applied in the same launch (§3.2, sub-4.3 b/w): 16-byte
+ *              entries, the record plus the block's slot in its tile in bits
+ *              [106, 128).
  *   GOLAY70    9-byte record: class | gain | 12-bit codeword message | a 2-bit
  *              in-class code per coordinate; blocks the 2-bit code cannot hold
  *              are exceptions as in PLANES12X (§3.2, 3.6 b/w).
@@ -255,9 +257,10 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
                        const float* group_centroids, const uint16_t* d_x, float* d_y,
                        void* stream);
 
-/* How GOLAY70 GEMVs enqueued from this call on (process-wide) decode the
- * blocks the 2-bit code cannot hold (§3.2 "Golay70": a plain decoder and one
- * that hoists work out of the per-slot path).
+/* How PLANES12X and GOLAY70 GEMVs enqueued from this call on (process-wide)
+ * decode their exceptions, the blocks whose exact PLANES14 record sits in the
+ * side list (§3.2: Golay70's plain decoder and one that hoists work out of
+ * the per-slot path; Planes12x's correction of its five-level blocks).
  *   LEECH_EXC_HOISTED (default): each workgroup first decodes its tile's
  *     exception records densely and keeps each one's contribution in LDS; the
  *     per-block loop then runs the Golay70 decode alone and an exception lane

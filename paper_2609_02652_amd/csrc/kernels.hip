@@ -115,7 +115,9 @@ struct GlobalSide {
     bits = *(const uint64_t*)ent;
     base = *(const uint32_t*)(ent + 8);
   }
-  // four-word window holding exception record ex (exact Planes14 record)
+  // four-word window holding exception record ex (exact Planes14 record) in a
+  // list of ES-byte entries
+  template <uint32_t ES>
   __device__ __forceinline__ void exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const;
 };
 struct LdsSide {
@@ -133,18 +135,21 @@ struct LdsSide {
     bits = *(const uint64_t*)ent;
     base = *(const uint32_t*)(ent + 8);
   }
+  template <uint32_t ES>
   __device__ __forceinline__ void exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const;
 };
 
+template <uint32_t ES>
 __device__ __forceinline__ void GlobalSide::exc_window(uint64_t ex, uint32_t w[4],
                                                       uint32_t& sh) const {
-  const uint64_t off = ex * kPlanes14Bytes;
+  const uint64_t off = ex * ES;
   const uint32_t* p = (const uint32_t*)(a->side0 + (off & ~3ull));
   w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
   sh = (uint32_t)(off & 2) * 8u;
 }
+template <uint32_t ES>
 __device__ __forceinline__ void LdsSide::exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const {
-  const uint64_t goff = ex * kPlanes14Bytes;
+  const uint64_t goff = ex * ES;
   if (exc_in_lds) {
     const uint32_t* p = (const uint32_t*)(exc + ((uint32_t)(goff - exc_start) & ~3u));
     w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
@@ -322,7 +327,7 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
     if (field) {      // five-level block: exact Planes14 record from the tile's list
       const uint64_t ex = (uint64_t)(side.p12_base(tile) + field - 1);
       uint32_t w[4], sh;
-      side.exc_window(ex, w, sh);
+      side.template exc_window<kP12EntryBytes>(ex, w, sh);
       planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
     } else {
       // two-plane level (0..3) -> code planes of level + 1, bit-parallel
@@ -353,7 +358,7 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
       side.unit_entry(a.side1, unit, bits, base);
       const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << ul) - 1ull));
       uint32_t w[4], sh;
-      side.exc_window(ex, w, sh);
+      side.template exc_window<kPlanes14Bytes>(ex, w, sh);
       planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
     } else {
       e16 = (r0 << 4) & 0x3FF0u;
@@ -531,6 +536,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   constexpr bool kW = LAYOUT != kNoWeights;
   constexpr bool kUnits = has_units<LAYOUT>();
   constexpr bool kExc = has_exc<LAYOUT>();
+  constexpr uint32_t kExcEntry = LAYOUT == LEECH_PLANES12X ? kP12EntryBytes : kPlanes14Bytes;
   const int64_t nb = a.nb;
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
   const int xblocks = groups * C;
@@ -543,8 +549,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if constexpr (kUnits) p += (size_t)groups * kUnitEntryBytes;
   uint8_t* exc_lds = p;                                                 // ≤ kExcLdsBytes
   if constexpr (kExc) p += kExcLdsBytes;
-  float* pre = (float*)p;                                               // Golay70: kPreFloats
-  if constexpr (LAYOUT == LEECH_GOLAY70) p += kPreFloats * 4;
+  float* pre = (float*)p;                                               // kPreFloats
+  if constexpr (kExc) p += kPreFloats * 4;
   float* red = (float*)p;                                               // waves × 64
 
   const int tid = threadIdx.x, nthr = blockDim.x;
@@ -596,11 +602,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       e0 = b0;
       e1 = tile + 1 < a.tiles ? b1 : a.n_exc;
     }
-    side.exc_start = (e0 * kPlanes14Bytes) & ~15ull;
-    // the window of record e is 16 bytes from (14·e) & ~3, so the tile's
-    // windows end by 14·e1 + 2; rounded up to 16 this stays inside side0's
-    // 16 bytes of padding
-    const uint64_t end = e1 * kPlanes14Bytes + 2;
+    // Golay70's list holds 14-byte records: the window of record e is 16 bytes
+    // from (14·e) & ~3, so the tile's windows end by 14·e1 + 2, which rounded
+    // up to 16 stays inside side0's 16 bytes of padding; Planes12x's entries
+    // are 16 bytes, aligned
+    side.exc_start = (e0 * kExcEntry) & ~15ull;
+    const uint64_t end = e1 * kExcEntry + (kExcEntry == kPlanes14Bytes ? 2 : 0);
     exc_chunks = (end - side.exc_start + 15) / 16;
     side.exc_in_lds = exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
     exc_first = (uint32_t)e0;
@@ -675,18 +682,27 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       gr = __builtin_amdgcn_raw_buffer_load_b128(rg, tid * 16, 0, 0);
     }
   }
+  // the tile's unit entries and exception records: descriptors sized to the
+  // tile's data, and the null descriptor for a wave with nothing to stage, so
+  // that loads past the data reach no memory
   u32x4a ur[kUPer], er[kEPer];
   if constexpr (kUnits) {
+    const __amdgpu_buffer_rsrc_t ru =
+        make_rsrc(side_units + (uint64_t)tile * groups * kUnitEntryBytes,
+                  (uint64_t)groups * kUnitEntryBytes);
 #pragma unroll
-    for (int q = 0; q < kUPer; ++q)
-      ur[q] = ((const u32x4a*)side_units)[tile * groups + min(tid + q * nthr, groups - 1)];
+    for (int q = 0; q < kUPer; ++q) {
+      const __amdgpu_buffer_rsrc_t r = q * nthr + wave * 64 < groups ? ru : null_rsrc();
+      ur[q] = __builtin_amdgcn_raw_buffer_load_b128(r, (tid + q * nthr) * 16, 0, 0);
+    }
   }
   if constexpr (kExc) {
-    if (side.exc_in_lds) {
+    const uint64_t n_chunks = side.exc_in_lds ? exc_chunks : 0;
+    const __amdgpu_buffer_rsrc_t re = make_rsrc(a.side0 + side.exc_start, n_chunks * 16);
 #pragma unroll
-      for (int q = 0; q < kEPer; ++q)
-        er[q] = ((const u32x4a*)(a.side0 + side.exc_start))[min((int64_t)(tid + q * nthr),
-                                                                  (int64_t)exc_chunks - 1)];
+    for (int q = 0; q < kEPer; ++q) {
+      const __amdgpu_buffer_rsrc_t r = (uint64_t)(q * nthr + wave * 64) < n_chunks ? re : null_rsrc();
+      er[q] = __builtin_amdgcn_raw_buffer_load_b128(r, (tid + q * nthr) * 16, 0, 0);
     }
   }
   // the last column group: only its wave needs the data
@@ -741,39 +757,52 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
   auto cw = [&](uint32_t m) -> uint32_t { return golay_word(cws, m); };
 
-  // Golay70, hoisted decoder: the tile's exceptions (their exact Planes14
-  // records are in LDS) are decoded once, densely, before the loop, and each
-  // one's contribution dot12 · factor is kept in LDS; the loop then runs the
-  // Golay70 decode alone and a lane holding an exception takes the kept value
-  // in place of its own.  Same products, same order: y is unchanged.
+  // Hoisted exception decoder (Planes12x, Golay70): the tile's exceptions
+  // (their exact Planes14 records are in LDS) are decoded once, densely,
+  // before the loop, and each one's contribution dot12 · factor is kept in
+  // LDS; the loop then runs the layout's own decode alone and a lane holding
+  // an exception takes the kept value in place of its own.  Same products,
+  // same order: y is unchanged.
   bool hoisted = false;
-  if constexpr (LAYOUT == LEECH_GOLAY70) {
+  if constexpr (kExc) {
     hoisted = !a.inline_exc && side.exc_in_lds;
     if (hoisted) {
       for (uint32_t e = tid; e < exc_count; e += nthr) {
         const uint32_t ex = exc_first + e;
-        // its unit: the last one whose first exception index is ≤ ex
-        int lo = 0, hi = groups - 1;
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          uint64_t b;
+        uint32_t w[4], sh;
+        side.template exc_window<kExcEntry>(ex, w, sh);
+        int unit;
+        uint32_t ul;
+        if constexpr (LAYOUT == LEECH_PLANES12X) {
+          // the entry names the block's slot in the tile; units are R_t × C
+          // blocks in column order
+          const uint32_t slot = w[3] >> (kP12PosShift - 96);
+          unit = min((int)(slot / (uint32_t)(R_t * C)), gf);
+          ul = slot - (uint32_t)(unit * R_t * C);
+        } else {
+          // its unit: the last one whose first exception index is ≤ ex
+          int lo = 0, hi = groups - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            uint64_t b;
+            uint32_t base;
+            side.unit_entry(nullptr, tile * groups + mid, b, base);
+            if (base <= ex) lo = mid;
+            else hi = mid - 1;
+          }
+          uint64_t bits;
           uint32_t base;
-          side.unit_entry(nullptr, tile * groups + mid, b, base);
-          if (base <= ex) lo = mid;
-          else hi = mid - 1;
+          side.unit_entry(nullptr, tile * groups + lo, bits, base);
+          for (uint32_t k = ex - base; k; --k) bits &= bits - 1;   // its place in the unit
+          unit = lo;
+          ul = (uint32_t)__builtin_ctzll(bits);
         }
-        uint64_t bits;
-        uint32_t base;
-        side.unit_entry(nullptr, tile * groups + lo, bits, base);
-        for (uint32_t k = ex - base; k; --k) bits &= bits - 1;   // its place in the unit
-        const uint32_t ul = (uint32_t)__builtin_ctzll(bits);
-        const uint32_t cols = lo == gf ? (uint32_t)C_last : (uint32_t)C;
-        const uint32_t* xj = xs + 12 * (lo * C + ul % cols);
+        const uint32_t cols = unit == gf ? (uint32_t)C_last : (uint32_t)C;
+        const uint32_t* xj = xs + 12 * (unit * C + ul % cols);
         uint32_t xw[12];
 #pragma unroll
         for (int k = 0; k < 12; ++k) xw[k] = xj[k];
-        uint32_t w[4], sh, e16, p0, p1, p2, pos, h[12];
-        side.exc_window(ex, w, sh);
+        uint32_t e16, p0, p1, p2, pos, h[12];
         planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
         const LdsEntry te = tab(e16);
         planes_core(p0, p1, p2, pos, te.tlo, te.thi, h);
@@ -799,6 +828,23 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       acc += dot12(ones, xw);
     } else {
       uint32_t h[12], e16;
+      if constexpr (LAYOUT == LEECH_PLANES12X) {
+        if (hoisted) {
+          // two-plane level (0..3) -> code planes of level + 1, bit-parallel
+          e16 = (pr.w0 << 4) & 0x3FF0u;
+          const uint32_t pos = ~align(pr.w1, pr.w0, 10);
+          const uint32_t l0 = pr.w1 >> 2, l1 = align(pr.w2, pr.w1, 26);
+          const LdsEntry te = tab(e16);
+          planes_core(~l0, l0 ^ l1, l0 & l1, pos, te.tlo, te.thi, h);
+          float v = dot12(h, xw) * te.factor;
+          // the record's field is 1 + the block's index in the tile's list
+          const uint32_t field = pr.w2 >> kP12ExcShift;
+          const float kept = pre[min(field - 1u, exc_count)];
+          v = field && L.own ? kept : v;
+          acc = __builtin_fmaf((float)as_half(pr.scale), v, acc);
+          return;
+        }
+      }
       if constexpr (LAYOUT == LEECH_GOLAY70) {
         if (hoisted) {
           const uint32_t r0 = align(pr.w1, pr.w0, pr.sh), r1 = align(pr.w2, pr.w1, pr.sh);
@@ -1012,7 +1058,7 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
          (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
          (has_exc<LAYOUT>() ? kExcLdsBytes : 0) +
-         (LAYOUT == LEECH_GOLAY70 ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
+         (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
 }
 
 template <int LAYOUT, bool EVEN>

@@ -36,7 +36,12 @@ constexpr int kSlot32Large = 20;     // 5 levels
 constexpr int kUnitEntryBytes = 16;  // per-unit side entry: u64 bitmap, u32 base, u32 zero
 
 // Planes12x: the spare bits [82, 96) of the 12-byte record hold 1 + the
-// block's index in its tile's exception list, or 0.
+// block's index in its tile's exception list, or 0.  An exception entry is 16
+// bytes: the block's exact Planes14 record (14 bytes, bits [106, 112) zero)
+// with the block's storage slot inside its tile in bits [106, 128).
+constexpr int kP12EntryBytes = 16;
+constexpr int kP12PosShift = 106;
+constexpr int kP12PosBits = 22;
 constexpr int kP12ExcShift = 82 - 64;          // bit position inside word 2
 constexpr uint32_t kP12ExcMax = (1u << 14) - 2; // largest storable local index
 

@@ -115,7 +115,7 @@ def test_record_sizes_and_exceptions(cb):
     assert d14.served_bytes == d14.main_bytes + 2 * n
     d12 = P.expand_layout(cb, P.PLANES12X, cls, inp.gain, sm, lv)[0]
     assert d12.n_exceptions == five
-    assert d12.main_bytes == 12 * n + 16 and d12.side_bytes[0] == 14 * five + 16
+    assert d12.main_bytes == 12 * n + 16 and d12.side_bytes[0] == 16 * five + 16
     assert d12.side_bytes[1] == 4 * ((256 + 63 // d12.lane_cols) // (64 // d12.lane_cols))
     ds = P.expand_layout(cb, P.SLOT32, cls, inp.gain, sm, lv)[0]
     assert ds.main_bytes == 16 * n + 4 * five + 16
