@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--no-layer", action="store_true",
                     help="skip the 8B-layer comparison (separate vs fused launches vs FP16)")
     ap.add_argument("--layer-steps", type=int, default=300)
+    ap.add_argument("--no-batch", action="store_true",
+                    help="skip the batched GEMV sweep (B = 1, 2, 4, 8, 16)")
     ap.add_argument("--no-step14b", action="store_true",
                     help="skip the 14B-class decode step (40 layers + fp16 head, Leech vs FP16)")
     ap.add_argument("--step14b-layers", type=int, default=40)
@@ -67,8 +69,9 @@ def parse():
 class Arm:
     """One arm: a list of replica launchers, each enqueueing one GEMV."""
 
-    def __init__(self, name, launchers, served_bytes, desc=None):
+    def __init__(self, name, launchers, served_bytes, desc=None, mats=None):
         self.name, self.launchers, self.served_bytes, self.desc = name, launchers, served_bytes, desc
+        self.mats = mats
         self._graphs = {}
 
     def run(self, k, start=0):
@@ -111,7 +114,7 @@ def build_arms(args, torch, P, synth):
         mats = [mat] + [P.LeechMatrix(mat.desc, mat.main.clone(), mat.side0.clone(),
                                       mat.side1.clone(), mat.scale.clone(), dcb)
                         for _ in range(reps - 1)]
-        arms[name] = Arm(name, [(lambda m=m: m.gemv(x, y)) for m in mats], served, mat.desc)
+        arms[name] = Arm(name, [(lambda m=m: m.gemv(x, y)) for m in mats], served, mat.desc, mats)
         if name == "planes14":
             base_desc, mat14 = mat.desc, mat
         if name in ("planes12x", "golay70") and f"{name}_inline" in wanted:
@@ -136,7 +139,7 @@ def build_arms(args, torch, P, synth):
         served = W.numel() * 2
         reps = max(1, math.ceil(REPLICA_BYTES / served))
         Ws = [W] + [W.clone() for _ in range(reps - 1)]
-        arms["fp16"] = Arm("fp16", [(lambda w=w: P.fp16_gemv(w, x, y)) for w in Ws], served)
+        arms["fp16"] = Arm("fp16", [(lambda w=w: P.fp16_gemv(w, x, y)) for w in Ws], served, None, Ws)
         log(f"[bench] fp16: {served} bytes/GEMV, {reps} replicas")
     if "noweights" in wanted:
         arms["noweights"] = Arm("noweights", [lambda: P.noweights_ctrl(base_desc, x, y)], 0)
@@ -490,6 +493,49 @@ def bench_transcode(torch, P, dcb, parts, dev):
             "host_s_for_4B_model_blocks": round(BLOCKS_4B / blocks * host_s, 2)}
 
 
+def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
+    """Batched GEMV (§6 "Batching") on the bench workload in Planes14: µs per
+    launch of Y = W X for B activations (each block decoded once for up to 8
+    of them), walking the same replicas as the Planes14 arm; beside it the
+    FP16 weights through the library GEMM (torch.matmul, hipBLASLt) on the
+    same B, as the batched FP16 reference."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    p14 = arms["planes14"]
+    reps = len(p14.launchers)
+    leech = p14.mats
+    res = {}
+    fp = arms.get("fp16")
+    for B in batches:
+        X = torch.from_numpy(np.stack([synth.make_activation(inp.K, seed=50 + b, name="bench-batch")
+                                       for b in range(B)])).to(dev)
+        Y = torch.empty((B, inp.M), dtype=torch.float32, device=dev)
+        us = replay_us(torch, lambda i: leech[i % reps].gemv_batch(X, Y), args.layer_steps)
+        row = {"us": round(us, 2), "us_per_vector": round(us / B, 3),
+               "weight_GBps": round(p14.served_bytes / (us * 1e-6) / 1e9, 1)}
+        if fp is not None:
+            Ws = fp.mats
+            Xt = X.t().contiguous()
+            Yf = torch.empty((inp.M, B), dtype=torch.float16, device=dev)
+            # eager launches: the library GEMM is kept out of graph capture
+            for i in range(10):
+                torch.matmul(Ws[i % len(Ws)], Xt, out=Yf)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(args.layer_steps):
+                torch.matmul(Ws[i % len(Ws)], Xt, out=Yf)
+            e1.record()
+            torch.cuda.synchronize()
+            us_fp = e0.elapsed_time(e1) * 1e3 / args.layer_steps
+            row["fp16_gemm_us"] = round(us_fp, 2)
+            row["fp16_vs_planes14"] = round(us_fp / us, 3)
+        res[f"B{B}"] = row
+        log(f"[bench] batch B={B}: {row}")
+    return res
+
+
 def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
     """µs per activation rotation (blockwise Walsh–Hadamard, fp16 in and out)
     at the 8B and 14B site widths: one graph replay of args.layer_steps
@@ -629,6 +675,9 @@ def main():
             row["vs_fp16"] = round(statistics.median(ratios), 3)
         table[n] = row
 
+    batch = None
+    if not args.no_batch:
+        batch = bench_batch(args, torch, P, synth, inp, arms)
     layer = None
     if not args.no_layer:
         for a in arms.values():
@@ -672,6 +721,7 @@ def main():
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config)},
         "arms": table,
+        "batch": batch,
         "layer_8b": layer,
         "step_14b": step14b,
         "cpu_baseline": cpu,

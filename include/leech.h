@@ -241,6 +241,20 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
                const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
                float* d_y, void* stream);
 
+/* Batched GEMV (§6 "Batching": one decode of each weight serves several
+ * activations): Y[b] = W X[b] for b < batch, X[b] binary16 [Kpad] at
+ * d_X + b·ldx, Y[b] f32 [M] at d_Y + b·ldy.  Each block is decoded once per
+ * launch and multiplied with up to 8 activations staged in LDS; larger
+ * batches run in chunks of 8 (fewer where Kpad leaves too little LDS).  Every
+ * Y[b] is bit-identical to leech_gemv on X[b].  batch > 1 serves
+ * LEECH_PLANES14 (LEECH_E_LAYOUT otherwise) and needs ldx ≥ Kpad, ldx a
+ * multiple of 8 and ldy ≥ M (LEECH_E_ARG); batch = 1 is leech_gemv.  Other
+ * arguments as leech_gemv. */
+int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                     const void* d_side1, const void* d_class_table, const void* d_codewords,
+                     const uint16_t* d_scale, const float centroid[2], int batch,
+                     const uint16_t* d_X, int64_t ldx, float* d_Y, int64_t ldy, void* stream);
+
 /* Row-grouped GEMV (§3.4: q/k/v and gate/up fused into row-concatenated
  * launches): W is the row concatenation of n_groups matrices sharing one
  * activation, expanded as one layout of M = Σ group_rows rows; group g's rows

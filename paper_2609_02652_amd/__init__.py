@@ -118,6 +118,23 @@ class LeechMatrix:
                   self.scale.data_ptr(), centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
         return y
 
+    def gemv_batch(self, X, Y=None, centroids=(1.0, 1.0), stream=None):
+        """Y[b] = W X[b]: X fp16 [B, Kpad] device tensor (row stride a multiple
+        of 8), Y f32 [B, M]; each block decoded once for up to 8 activations."""
+        torch = _torch()
+        if X.dtype != torch.float16 or X.dim() != 2 or X.shape[1] != self.Kpad or X.stride(1) != 1:
+            raise ValueError("X must be an fp16 [B, Kpad] tensor with unit column stride")
+        B = X.shape[0]
+        if Y is None:
+            Y = torch.empty((B, self.M), dtype=torch.float32, device=X.device)
+        elif Y.dtype != torch.float32 or Y.shape != (B, self.M) or Y.stride(1) != 1:
+            raise ValueError("Y must be an f32 [B, M] tensor with unit column stride")
+        m, s0, s1 = self._ptrs()
+        _lib.gemv_batch(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
+                        self.dcb.golay_gen.data_ptr(), self.scale.data_ptr(), centroids, B,
+                        X.data_ptr(), X.stride(0), Y.data_ptr(), Y.stride(0), _stream(stream))
+        return Y
+
     def gemv_grouped(self, x, group_rows, group_centroids, y=None, stream=None):
         """y = W x for a row concatenation of matrices sharing x (§3.4): group g
         covers the next group_rows[g] rows and uses gain centroids

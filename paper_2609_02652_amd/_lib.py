@@ -28,7 +28,7 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_host_decode_layout", "leech_gemv", "leech_gemv_grouped", "leech_decode_blocks",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
-           "leech_transcode_planes14", "leech_set_exception_mode"]
+           "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch"]
 
 
 class LeechError(RuntimeError):
@@ -79,6 +79,8 @@ def _load() -> C.CDLL:
         "leech_planes14_desc": (I, [I64, I64, C.POINTER(LayoutDesc)]),
         "leech_transcode_planes14": (I, [C.POINTER(LayoutDesc), P, P, P, P, P]),
         "leech_set_exception_mode": (I, [I]),
+        "leech_gemv_batch": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, I, P, I64, P, I64,
+                                 P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -234,6 +236,14 @@ def gemv(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroid
     check(lib.leech_gemv(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
                          d_codewords or None, d_scale, C.cast(cen, C.c_void_p), d_x, d_y,
                          stream or None))
+
+
+def gemv_batch(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroids, batch,
+               d_X, ldx, d_Y, ldy, stream=0):
+    cen = (C.c_float * 2)(float(centroids[0]), float(centroids[1]))
+    check(lib.leech_gemv_batch(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
+                               d_codewords or None, d_scale, C.cast(cen, C.c_void_p), batch, d_X,
+                               ldx, d_Y, ldy, stream or None))
 
 
 MAX_GROUPS = 8

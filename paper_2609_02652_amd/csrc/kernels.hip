@@ -99,7 +99,11 @@ struct GemvArgs {
   int ngroups;
   int64_t grp_end[LEECH_MAX_GROUPS];      // first row past each group
   float grp_cen[LEECH_MAX_GROUPS][2];
-  int inline_exc;               // Golay70: 1 = exceptions decoded in the loop
+  int inline_exc;               // Planes12x, Golay70: 1 = exceptions decoded in the loop
+  // batched launches: activation b at x + b·ldx, output b at y + b·ldy, for
+  // b < nbatch (≤ the kernel's batch width)
+  int64_t ldx, ldy;
+  int nbatch;
 };
 
 // Where side data comes from: global memory (verification decode, and the
@@ -529,7 +533,10 @@ __host__ __device__ constexpr bool has_exc() {
   return LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
 }
 
-template <int LAYOUT, bool EVEN>
+// NB: batch width.  Each decoded block is multiplied with NB activations
+// (NB > 1: Planes14), in the same order as a single GEMV, so every output
+// vector is bit-identical to that activation's own GEMV.
+template <int LAYOUT, bool EVEN, int NB = 1>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ __attribute__((aligned(16))) LdsEntry ts[1024];
@@ -540,8 +547,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const int64_t nb = a.nb;
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
   const int xblocks = groups * C;
-  uint32_t* xs = (uint32_t*)smem;                                       // xblocks × 12 x pairs
-  uint8_t* p = smem + (size_t)xblocks * 48;
+  uint32_t* xs = (uint32_t*)smem;                                  // NB × xblocks × 12 x pairs
+  uint8_t* p = smem + (size_t)NB * xblocks * 48;
   G70Entry* gs = (G70Entry*)p;                                          // Golay70: 301 entries
   uint32_t* cws = (uint32_t*)(p + kG70Entries * sizeof(G70Entry));      // 128 words
   if constexpr (LAYOUT == LEECH_GOLAY70) p += kG70LdsBytes;
@@ -624,9 +631,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // classes): loads of unknown count here, before the ordered ones.  Only the
   // ball's class ids occur in a layout, so only their entries are staged, both
   // gain entries of a class from one read of its table record.
-  for (int j = tid + kXPer * nthr; j < xblocks; j += nthr) {
-    if (j < nb) {
-      store_x_block(load_x_block(a.x + 24 * (int64_t)j), xs + 12 * j);
+  // (a batched launch stages all its activations here: vector b's blocks
+  // follow vector b − 1's, zero past nb and for vectors past nbatch)
+  for (int j = NB == 1 ? tid + kXPer * nthr : tid; j < NB * xblocks; j += nthr) {
+    const int b = NB == 1 ? 0 : j / xblocks, jb = j - b * xblocks;
+    if (jb < nb && b < a.nbatch) {
+      store_x_block(load_x_block(a.x + b * a.ldx + 24 * (int64_t)jb), xs + 12 * j);
     } else {
       u32x4a* d = (u32x4a*)(xs + 12 * j);
       d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
@@ -662,7 +672,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   XBlock xr[kXPer];
 #pragma unroll
   for (int q = 0; q < kXPer; ++q) {
-    const bool live = q * nthr + wave * 64 < nb;
+    const bool live = NB == 1 && q * nthr + wave * 64 < nb;
     const int off = (tid + q * nthr) * 48;
     const __amdgpu_buffer_rsrc_t r = live ? rs_x : null_rsrc();
     xr[q].v0 = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
@@ -716,10 +726,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     pf[d] = load_unit<LAYOUT, EVEN>(a, t, d < units, Lp, min(wave + d * waves, g_stand), gside);
     __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
   }
+  if constexpr (NB == 1) {
 #pragma unroll
-  for (int q = 0; q < kXPer; ++q) {
-    const int j = tid + q * nthr;
-    if (j < xblocks) store_x_block(xr[q], xs + 12 * j);
+    for (int q = 0; q < kXPer; ++q) {
+      const int j = tid + q * nthr;
+      if (j < xblocks) store_x_block(xr[q], xs + 12 * j);
+    }
   }
   if constexpr (kW) {
     if (tid < kBallClasses) {
@@ -814,7 +826,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   }
 
   const uint8_t* x_lane = (const uint8_t*)xs + __umul24(cl, 48u);
-  float acc = 0.0f;
+  float acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = 0.0f;
   // One unit: decode slot p for unit g and accumulate.
   auto process = [&](const Pref& pr, int g, const Lane& L) {
     const u32x4a* xp = (const u32x4a*)(x_lane + g * (C * 48));
@@ -825,7 +839,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       const uint32_t ones[12] = {0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u,
                                  0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u,
                                  0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
-      acc += dot12(ones, xw);
+      acc[0] += dot12(ones, xw);
     } else {
       uint32_t h[12], e16;
       if constexpr (LAYOUT == LEECH_PLANES12X) {
@@ -841,7 +855,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
           const uint32_t field = pr.w2 >> kP12ExcShift;
           const float kept = pre[min(field - 1u, exc_count)];
           v = field && L.own ? kept : v;
-          acc = __builtin_fmaf((float)as_half(pr.scale), v, acc);
+          acc[0] = __builtin_fmaf((float)as_half(pr.scale), v, acc[0]);
           return;
         }
       }
@@ -862,13 +876,21 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
           // zero, not the contribution kept for the block it stands in for
           const float kept = pre[min(ei, exc_count)];
           v = ((r2 >> 6) & 1u) && L.own ? kept : v;
-          acc = __builtin_fmaf((float)as_half(pr.scale), v, acc);
+          acc[0] = __builtin_fmaf((float)as_half(pr.scale), v, acc[0]);
           return;
         }
       }
       decode_block<LAYOUT>(pr, L.ul, tile, tile * groups + g, tab, g70, cw, side, a, h, e16);
-      const float s = dot12(h, xw);
-      acc = __builtin_fmaf((float)as_half(pr.scale), s * tab(e16).factor, acc);
+      const float sc = (float)as_half(pr.scale), f = tab(e16).factor;
+      acc[0] = __builtin_fmaf(sc, dot12(h, xw) * f, acc[0]);
+#pragma unroll
+      for (int b = 1; b < NB; ++b) {
+        const u32x4a* xq = xp + 3 * b * xblocks;
+        const u32x4a y0 = xq[0], y1 = xq[1], y2 = xq[2];
+        const uint32_t xv[12] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w,
+                                 y2.x, y2.y, y2.z, y2.w};
+        acc[b] = __builtin_fmaf(sc, dot12(h, xv) * f, acc[b]);
+      }
     }
   };
   int done = 0;
@@ -894,13 +916,20 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // the last column group, by the wave next in turn; its lanes past the last
   // column read zero x and add exactly zero
   if (wave == w_last) process(plast, gf, Ll);
-  for (int off = 1; off < C; off <<= 1) acc += __shfl_xor(acc, off);
-  if (cl == 0 && rl < R_t) red[wave * 64 + rl] = acc;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    float v = acc[b];
+    for (int off = 1; off < C; off <<= 1) v += __shfl_xor(v, off);
+    if (cl == 0 && rl < R_t) red[(b * waves + wave) * 64 + rl] = v;
+  }
   __syncthreads();
-  if (tid < R_t) {
-    float y = 0.0f;
-    for (int w = 0; w < waves; ++w) y += red[w * 64 + tid];
-    a.y[(int64_t)tile * a.R + tid] = y;
+  for (int i = tid; i < NB * 64; i += nthr) {
+    const int b = i >> 6, row = i & 63;
+    if (row < R_t && b < a.nbatch) {
+      float y = 0.0f;
+      for (int w = 0; w < waves; ++w) y += red[(b * waves + w) * 64 + row];
+      a.y[b * a.ldy + (int64_t)tile * a.R + row] = y;
+    }
   }
 }
 
@@ -1039,6 +1068,7 @@ static GemvArgs make_args(const leech_layout_desc* d) {
   a.tiles = (d->M + a.R - 1) / a.R;
   a.n_exc = d->n_exceptions;
   a.main_bytes = d->main_bytes;
+  a.nbatch = 1;
   return a;
 }
 
@@ -1052,36 +1082,50 @@ static bool even_bases(const GemvArgs& a, int layout) {
   return (rows_last * a.C * stride) % 4 == 0;
 }
 
-template <int LAYOUT>
+template <int LAYOUT, int NB = 1>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
-  return (size_t)a.groups * a.C * 48 +
+  return (size_t)NB * a.groups * a.C * 48 + (size_t)(NB - 1) * a.waves * 64 * 4 +
          (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
          (has_exc<LAYOUT>() ? kExcLdsBytes : 0) +
          (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
 }
 
-template <int LAYOUT, bool EVEN>
+template <int LAYOUT, bool EVEN, int NB = 1>
 static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
   if (shmem + kTableBytes > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN, NB>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN>), dim3((unsigned)a.tiles), dim3(64 * a.waves),
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB>), dim3((unsigned)a.tiles), dim3(64 * a.waves),
                      shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
   return LEECH_OK;
 }
 
-template <int LAYOUT>
+template <int LAYOUT, int NB = 1>
 static int launch_gemv(const GemvArgs& a, hipStream_t st) {
-  const size_t shmem = gemv_lds_bytes<LAYOUT>(a);
+  const size_t shmem = gemv_lds_bytes<LAYOUT, NB>(a);
   if (shmem + kTableBytes > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
-  if (LAYOUT == kNoWeights || even_bases(a, LAYOUT)) return launch_gemv_as<LAYOUT, true>(a, shmem, st);
-  return launch_gemv_as<LAYOUT, false>(a, shmem, st);
+  if (LAYOUT == kNoWeights || even_bases(a, LAYOUT))
+    return launch_gemv_as<LAYOUT, true, NB>(a, shmem, st);
+  return launch_gemv_as<LAYOUT, false, NB>(a, shmem, st);
+}
+
+// Batch width of the next chunk of a batched launch: 2, 4 or 8 (the next
+// power of two at or above the vectors left, at most 8; vectors past the
+// chunk's count read zero), narrowed until the activations fit in LDS; 1 for
+// a single vector left, or when not even two fit.
+static int batch_width(const GemvArgs& a, int left) {
+  if (left <= 1) return 1;
+  const size_t one = gemv_lds_bytes<LEECH_PLANES14>(a);
+  const size_t per = (size_t)a.groups * a.C * 48 + (size_t)a.waves * 64 * 4;
+  for (int w = left > 4 ? 8 : left > 2 ? 4 : 2; w >= 2; w >>= 1)
+    if (one + (size_t)(w - 1) * per + kTableBytes <= 160 * 1024) return w;
+  return 1;
 }
 
 template <int LAYOUT>
@@ -1152,6 +1196,42 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
   a.cen0 = centroid[0];
   a.cen1 = centroid[1];
   return gemv_dispatch(desc, a, (hipStream_t)stream);
+}
+
+int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                     const void* d_side1, const void* d_class_table, const void* d_codewords,
+                     const uint16_t* d_scale, const float centroid[2], int batch,
+                     const uint16_t* d_X, int64_t ldx, float* d_Y, int64_t ldy, void* stream) {
+  clear_error();
+  if (!centroid) return set_error(LEECH_E_ARG, "NULL argument");
+  if (batch < 1) return set_error(LEECH_E_ARG, "batch must be at least 1");
+  GemvArgs a;
+  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_X,
+                      d_Y, &a);
+  if (rc) return rc;
+  if (batch > 1 && desc->layout != LEECH_PLANES14)
+    return set_error(LEECH_E_LAYOUT, "batched GEMVs serve the PLANES14 layout");
+  if (batch > 1 && (ldx < desc->Kpad || ldx % 8 || ldy < desc->M))
+    return set_error(LEECH_E_ARG, "need ldx >= Kpad, ldx a multiple of 8, ldy >= M");
+  a.cen0 = centroid[0];
+  a.cen1 = centroid[1];
+  a.ldx = ldx;
+  a.ldy = ldy;
+  const hipStream_t st = (hipStream_t)stream;
+  for (int b0 = 0; b0 < batch;) {
+    const int w = batch_width(a, batch - b0);
+    GemvArgs c = a;
+    c.x = d_X + (int64_t)b0 * ldx;
+    c.y = d_Y + (int64_t)b0 * ldy;
+    c.nbatch = std::min(w, batch - b0);
+    rc = w == 8   ? launch_gemv<LEECH_PLANES14, 8>(c, st)
+         : w == 4 ? launch_gemv<LEECH_PLANES14, 4>(c, st)
+         : w == 2 ? launch_gemv<LEECH_PLANES14, 2>(c, st)
+                  : gemv_dispatch(desc, c, st);
+    if (rc) return rc;
+    b0 += c.nbatch;
+  }
+  return LEECH_OK;
 }
 
 int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const void* d_side0,

@@ -218,6 +218,27 @@ def test_grouped_gemv_validates_groups_before_launch():
         assert e.value.code == code, (rows, cens, _lib.lib.leech_last_error())
 
 
+def test_batch_gemv_validates_before_launch():
+    """Batch arguments are checked on the host before any launch (stand-in
+    device pointers, never dereferenced)."""
+    d = P.LayoutDesc()
+    d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 128, 48, 2
+    d.lane_cols = 16
+    fake = 256
+    cases = [
+        (P.PLANES14, 0, 48, 128, -1),       # empty batch
+        (P.PLANES14, 2, 40, 128, -1),       # ldx below Kpad
+        (P.PLANES14, 2, 52, 128, -1),       # ldx not a multiple of 8
+        (P.PLANES14, 2, 48, 100, -1),       # ldy below M
+        (P.GOLAY70, 2, 48, 128, -2),        # batched launches serve Planes14
+    ]
+    for layout, batch, ldx, ldy, code in cases:
+        d.layout = layout
+        with pytest.raises(P.LeechError) as e:
+            _lib.gemv_batch(d, fake, 0, 0, fake, fake, fake, (1, 1), batch, fake, ldx, fake, ldy)
+        assert e.value.code == code, (layout, batch, ldx, ldy, _lib.lib.leech_last_error())
+
+
 def test_rotate_validates_before_launch():
     fake = 256
     for K, Kpad, code in ((0, 24, -3), (48, 24, -3), (65536, 65544, -3)):
