@@ -128,13 +128,16 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *   SLOT32     one-hot level masks (§3.2): class | gain | sign mask | one 24-bit
  *              mask per level above level 0; 16-byte records (≤ 4 levels) or
  *              20-byte records (5 levels); a side table locates each record.
- *   PLANES14   three binary bit planes (§2.2, §2.3): a 112-bit record at a
- *              uniform 14-byte stride; the served layout, 4.80 b/w.  Bits
- *              (little-endian from the record's first byte): p0 [0,24),
- *              pos[0,8) [24,32), p1 [32,56), pos[8,16) [56,64), p2 [64,88),
- *              pos[16,24) [88,96), class [96,105), gain 105, zero [106,112);
- *              p0|p1<<1|p2<<2 of coordinate i is its level + 1 and pos is the
- *              inverted sign mask (bit i set iff z_i ≥ 0).
+ *   PLANES14   three binary bit planes and the sign plane (§2.2, §2.3) in a
+ *              112-bit record at a uniform 14-byte stride; the served layout,
+ *              4.80 b/w.  With p0|p1<<1|p2<<2 of coordinate i its level + 1
+ *              and pos the inverted sign mask (bit i set iff z_i ≥ 0), the
+ *              planes are stored sliced by nibble: word w_r (r = 0..3, 24
+ *              bits) holds in bits [4g, 4g+4) the bits p0, p1, p2, pos of
+ *              coordinate 4g + r.  Bits (little-endian from the record's
+ *              first byte): w0 [0,24), w3[0,8) [24,32), w1 [32,56),
+ *              w3[8,16) [56,64), w2 [64,88), w3[16,24) [88,96),
+ *              class [96,105), gain 105, zero [106,112).
  *   PLANES12X  two bit planes in a 12-byte record for every block; blocks with
  *              five levels also keep their exact PLANES14 record in an exception
  *              table applied in the same launch (§3.2, sub-4.3 b/w): 16-byte

@@ -233,10 +233,10 @@ __device__ __forceinline__ void pair_sources(uint32_t N, uint32_t s[3]) {
 // when not (v_perm's selector 8 replicates bit 7 of table byte 1, a magnitude
 // below 0x80, giving 0x00).  Pair 3r + k of h[] covers the coordinates listed
 // by pair_sources.
-__device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t pos,
-                                            uint32_t tlo, uint32_t thi, uint32_t h[12]) {
-  uint32_t n[4];
-  nibble_transpose(p0, p1, p2, pos, n);
+// Nibble core: the four nibble words of a block (as a Planes14 record stores
+// them) -> 12 binary16 pairs.
+__device__ __forceinline__ void nibble_core(const uint32_t n[4], uint32_t tlo, uint32_t thi,
+                                            uint32_t h[12]) {
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     uint32_t s[3];
@@ -244,6 +244,12 @@ __device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p
 #pragma unroll
     for (int k = 0; k < 3; ++k) h[3 * r + k] = perm(thi, tlo, s[k] & 0x08070807u);
   }
+}
+__device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t pos,
+                                            uint32_t tlo, uint32_t thi, uint32_t h[12]) {
+  uint32_t n[4];
+  nibble_transpose(p0, p1, p2, pos, n);
+  nibble_core(n, tlo, thi, h);
 }
 
 // Golay70 core: nibble (c0, c1, side, 0) -> index side·4 + code; the low half
@@ -300,10 +306,10 @@ struct Pref {
 };
 
 // Planes14 fields of the four-word window whose record starts at bit sh (0 or
-// 16): every plane starts on a 32-bit boundary of the record, so one funnel
-// shift each gives p0, p1, p2 in bits 0..23 with one byte of the inverted sign
-// mask above; two byte permutes gather that mask.  e16 = (class | gain << 9)·16,
-// the entry's LDS byte address.
+// 16): every nibble word starts on a 32-bit boundary of the record, so one
+// funnel shift each gives w0, w1, w2 in bits 0..23 with one byte of w3 above;
+// two byte permutes gather w3.  e16 = (class | gain << 9)·16, the entry's LDS
+// byte address.  The words are already sliced by nibble: no transpose.
 __device__ __forceinline__ void planes14_fields(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
                                                 uint32_t sh, uint32_t esh, uint32_t& e16,
                                                 uint32_t& p0, uint32_t& p1, uint32_t& p2,
@@ -324,15 +330,25 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
                                              TAB tab, G70 g70, CW cw, const SIDE& side,
                                              const GemvArgs& a, uint32_t h[12], uint32_t& e16) {
   uint32_t p0 = 0, p1 = 0, p2 = 0, pos = 0;
+  // a Planes14 record (the layout's own, or an exception's exact record)
+  auto planes14 = [&](uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t sh,
+                      uint32_t esh) {
+    uint32_t n[4];
+    planes14_fields(w0, w1, w2, w3, sh, esh, e16, n[0], n[1], n[2], n[3]);
+    const LdsEntry t = tab(e16);
+    nibble_core(n, t.tlo, t.thi, h);
+  };
   if constexpr (LAYOUT == LEECH_PLANES14) {
-    planes14_fields(p.w0, p.w1, p.w2, p.w3, p.sh, p.esh, e16, p0, p1, p2, pos);
+    planes14(p.w0, p.w1, p.w2, p.w3, p.sh, p.esh);
+    return;
   } else if constexpr (LAYOUT == LEECH_PLANES12X) {
     const uint32_t field = p.w2 >> kP12ExcShift;
     if (field) {      // five-level block: exact Planes14 record from the tile's list
       const uint64_t ex = (uint64_t)(side.p12_base(tile) + field - 1);
       uint32_t w[4], sh;
       side.template exc_window<kP12EntryBytes>(ex, w, sh);
-      planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
+      planes14(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u);
+      return;
     } else {
       // two-plane level (0..3) -> code planes of level + 1, bit-parallel
       e16 = (p.w0 << 4) & 0x3FF0u;
@@ -363,7 +379,8 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
       const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << ul) - 1ull));
       uint32_t w[4], sh;
       side.template exc_window<kPlanes14Bytes>(ex, w, sh);
-      planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
+      planes14(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u);
+      return;
     } else {
       e16 = (r0 << 4) & 0x3FF0u;
       const uint32_t side_bits = cw((r0 >> 10) & 0xFFFu);
@@ -814,10 +831,10 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         uint32_t xw[12];
 #pragma unroll
         for (int k = 0; k < 12; ++k) xw[k] = xj[k];
-        uint32_t e16, p0, p1, p2, pos, h[12];
-        planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, p0, p1, p2, pos);
+        uint32_t e16, n[4], h[12];
+        planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, n[0], n[1], n[2], n[3]);
         const LdsEntry te = tab(e16);
-        planes_core(p0, p1, p2, pos, te.tlo, te.thi, h);
+        nibble_core(n, te.tlo, te.thi, h);
         pre[e] = dot12(h, xw) * te.factor;
       }
       if (tid == 0) pre[exc_count] = 0.0f;

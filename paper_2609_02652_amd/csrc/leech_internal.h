@@ -25,8 +25,10 @@ constexpr int kPadBytes = 16;        // trailing zero bytes after every record s
 
 // Record widths of the four layouts (bytes).
 constexpr int kPlanes14Bytes = 14;
-// Planes14 bit positions: planes p0, p1, p2 at 0, 32, 64, each followed by one
-// byte of the inverted sign mask; class (9 bits) and gain bit from bit 96.
+// Planes14 bit positions: nibble words w0, w1, w2 at 0, 32, 64, each followed
+// by one byte of w3; class (9 bits) and gain bit from bit 96.  Word w_r holds
+// in bits [4g, 4g+4) the nibble of coordinate 4g + r: its level code (level
+// + 1) in bits 0..2 and 1 in bit 3 when the coordinate is not negative.
 constexpr int kP14PlanePos[3] = {0, 32, 64};
 constexpr int kP14ClassPos = 96;
 constexpr int kPlanes12Bytes = 12;
@@ -63,6 +65,22 @@ struct DevClass {
 };
 constexpr int kSignByteCode = 0;
 __host__ __device__ inline int level_code(int level) { return level + 1; }
+
+// The three level-code planes and the non-negative plane of a block as the
+// four Planes14 nibble words: bit q of nibble g of w[r] is bit 4g + r of
+// plane q (the four planes transposed by nibble).
+__host__ __device__ inline void planes_to_nibbles(uint32_t p0, uint32_t p1, uint32_t p2,
+                                                  uint32_t pos, uint32_t w[4]) {
+  for (int r = 0; r < 4; ++r) {
+    uint32_t v = 0;
+    for (int g = 0; g < 6; ++g) {
+      const int i = 4 * g + r;
+      v |= ((p0 >> i & 1u) | (p1 >> i & 1u) << 1 | (p2 >> i & 1u) << 2 | (pos >> i & 1u) << 3)
+           << (4 * g);
+    }
+    w[r] = v;
+  }
+}
 static_assert(sizeof(DevClass) == 32, "device class record is 32 bytes");
 
 // Geometry shared by the expansion and the kernels: rows are grouped into

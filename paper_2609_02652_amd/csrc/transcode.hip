@@ -9,8 +9,9 @@
 // wave-tile order, reads that block's 8-byte code (rows of a unit are nb
 // blocks apart, so these reads gather) and decodes it with the shared
 // format-v1 routines: a binary search over the class offsets, two or three
-// 64-bit divisions into the mixed-radix digits, and colex unranking of each
-// level's positions straight into the three level-code planes.  The index
+// 64-bit divisions into the mixed-radix digits, colex unranking of each
+// level's positions straight into the three level-code planes, and the planes
+// sliced into the record's nibble words.  The index
 // table (60 KiB) is read through the caches.  A grid-stride loop bounds the
 // grid; every thread leaves once its slots pass the end of the stream.
 
@@ -40,10 +41,10 @@ struct TranscodeArgs {
   int C, R;
 };
 
-// Record words of one block: p0 | pos[0:8) << 24, p1 | pos[8:16) << 24,
-// p2 | pos[16:24) << 24, and the 16-bit class | gain << 9 (the record's last
-// two bytes).  Zeros for slots past the matrix and for codes that are not
-// format-v1 codes.
+// Record words of one block: w0 | w3[0:8) << 24, w1 | w3[8:16) << 24,
+// w2 | w3[16:24) << 24 (the nibble words of the block's planes), and the
+// 16-bit class | gain << 9 (the record's last two bytes).  Zeros for slots
+// past the matrix and for codes that are not format-v1 codes.
 __device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, uint32_t w[4]) {
   w[0] = w[1] = w[2] = w[3] = 0;
   if (s >= a.n) return;
@@ -62,9 +63,10 @@ __device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, 
     atomicAdd(a.bad, 1u);
     return;
   }
-  const uint32_t pos = ~smask & 0xFFFFFFu;
+  uint32_t n[4];
+  planes_to_nibbles(p[0], p[1], p[2], ~smask & 0xFFFFFFu, n);
 #pragma unroll
-  for (int k = 0; k < 3; ++k) w[k] = p[k] | (pos >> (8 * k) & 0xFFu) << 24;
+  for (int k = 0; k < 3; ++k) w[k] = n[k] | (n[3] >> (8 * k) & 0xFFu) << 24;
   w[3] = (uint32_t)cls | (uint32_t)gain << 9;
 }
 
