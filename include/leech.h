@@ -130,14 +130,17 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *              20-byte records (5 levels); a side table locates each record.
  *   PLANES14   three binary bit planes and the sign plane (§2.2, §2.3) in a
  *              112-bit record at a uniform 14-byte stride; the served layout,
- *              4.80 b/w.  With p0|p1<<1|p2<<2 of coordinate i its level + 1
- *              and pos the inverted sign mask (bit i set iff z_i ≥ 0), the
- *              planes are stored sliced by nibble: word w_r (r = 0..3, 24
- *              bits) holds in bits [4g, 4g+4) the bits p0, p1, p2, pos of
- *              coordinate 4g + r.  Bits (little-endian from the record's
- *              first byte): w0 [0,24), w3[0,8) [24,32), w1 [32,56),
- *              w3[8,16) [56,64), w2 [64,88), w3[16,24) [88,96),
- *              class [96,105), gain 105, zero [106,112).
+ *              4.80 b/w.  Bits (little-endian from the record's first byte):
+ *              pair words W0 [0,32), W1 [32,64), W2 [64,96), class [96,105),
+ *              gain 105, zero [106,112).  With c_i = p0|p1<<1|p2<<2 of
+ *              coordinate i (its level + 1) and pos_i = 1 iff z_i ≥ 0, the
+ *              96 plane bits are stored in the GPU's consumption order: the
+ *              coordinates form 12 pairs (a_q, b_q) = (0,16), (4,20), (8,12),
+ *              (1,17), (5,21), (9,13), (2,18), (6,22), (10,14), (3,19),
+ *              (7,23), (11,15), and W_w rotated right by 4k and masked with
+ *              0x08070807 is c_a | pos_a << 11 | c_b << 16 | pos_b << 27 for
+ *              pair q = 4w + k (k = 0..3; the four rotations cover each bit
+ *              of W_w once).
  *   PLANES12X  two bit planes in a 12-byte record for every block; blocks with
  *              five levels also keep their exact PLANES14 record in an exception
  *              table applied in the same launch (§3.2, sub-4.3 b/w): 16-byte

@@ -305,20 +305,30 @@ struct Pref {
   uint32_t sh, esh;
 };
 
-// Planes14 fields of the four-word window whose record starts at bit sh (0 or
-// 16): every nibble word starts on a 32-bit boundary of the record, so one
-// funnel shift each gives w0, w1, w2 in bits 0..23 with one byte of w3 above;
-// two byte permutes gather w3.  e16 = (class | gain << 9)·16, the entry's LDS
-// byte address.  The words are already sliced by nibble: no transpose.
-__device__ __forceinline__ void planes14_fields(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
-                                                uint32_t sh, uint32_t esh, uint32_t& e16,
-                                                uint32_t& p0, uint32_t& p1, uint32_t& p2,
-                                                uint32_t& pos) {
-  p0 = align(w1, w0, sh);
-  p1 = align(w2, w1, sh);
-  p2 = align(w3, w2, sh);
-  pos = perm(p2, perm(p1, p0, 0x0C0C0703u), 0x0C070100u);
+// Planes14 record in the four-word window whose record starts at bit sh (0
+// or 16): each pair word starts on a 32-bit boundary of the record, so one
+// funnel shift each gives it; e16 = (class | gain << 9)·16, the entry's LDS
+// byte address.  Pair q = 4w + k of word w is its rotation by 4k masked with
+// 0x08070807, which is already the byte-permute selector of the pair's two
+// binary16 values (the store order of the record): no transpose, no pair
+// gathering.
+__device__ __forceinline__ void p14_record(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
+                                           uint32_t sh, uint32_t esh, uint32_t W[3],
+                                           uint32_t& e16) {
+  W[0] = align(w1, w0, sh);
+  W[1] = align(w2, w1, sh);
+  W[2] = align(w3, w2, sh);
   e16 = align(w3, w3, esh) & 0x3FF0u;
+}
+__device__ __forceinline__ void p14_core(const uint32_t W[3], uint32_t tlo, uint32_t thi,
+                                         uint32_t h[12]) {
+#pragma unroll
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t s = k ? align(W[w], W[w], 4 * k) : W[w];
+      h[4 * w + k] = perm(thi, tlo, s & 0x08070807u);
+    }
 }
 
 // Decode one block into 12 binary16 pairs and its table entry's byte address.
@@ -333,10 +343,10 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
   // a Planes14 record (the layout's own, or an exception's exact record)
   auto planes14 = [&](uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t sh,
                       uint32_t esh) {
-    uint32_t n[4];
-    planes14_fields(w0, w1, w2, w3, sh, esh, e16, n[0], n[1], n[2], n[3]);
+    uint32_t W[3];
+    p14_record(w0, w1, w2, w3, sh, esh, W, e16);
     const LdsEntry t = tab(e16);
-    nibble_core(n, t.tlo, t.thi, h);
+    p14_core(W, t.tlo, t.thi, h);
   };
   if constexpr (LAYOUT == LEECH_PLANES14) {
     planes14(p.w0, p.w1, p.w2, p.w3, p.sh, p.esh);
@@ -831,10 +841,10 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         uint32_t xw[12];
 #pragma unroll
         for (int k = 0; k < 12; ++k) xw[k] = xj[k];
-        uint32_t e16, n[4], h[12];
-        planes14_fields(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, e16, n[0], n[1], n[2], n[3]);
+        uint32_t e16, W[3], h[12];
+        p14_record(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, W, e16);
         const LdsEntry te = tab(e16);
-        nibble_core(n, te.tlo, te.thi, h);
+        p14_core(W, te.tlo, te.thi, h);
         pre[e] = dot12(h, xw) * te.factor;
       }
       if (tid == 0) pre[exc_count] = 0.0f;

@@ -25,12 +25,52 @@ constexpr int kPadBytes = 16;        // trailing zero bytes after every record s
 
 // Record widths of the four layouts (bytes).
 constexpr int kPlanes14Bytes = 14;
-// Planes14 bit positions: nibble words w0, w1, w2 at 0, 32, 64, each followed
-// by one byte of w3; class (9 bits) and gain bit from bit 96.  Word w_r holds
-// in bits [4g, 4g+4) the nibble of coordinate 4g + r: its level code (level
-// + 1) in bits 0..2 and 1 in bit 3 when the coordinate is not negative.
-constexpr int kP14PlanePos[3] = {0, 32, 64};
+// Planes14: three 32-bit pair words at bits 0, 32, 64, class (9 bits) and
+// gain bit from bit 96.  A block's 24 coordinates form the 12 pairs of
+// kPairCoords; pair q = 4w + k lies in word w: rotated right by 4k and masked
+// with 0x08070807, the word holds the level code (level + 1) of the pair's
+// first coordinate in bits 0..2 and its non-negative bit in bit 11, and the
+// second coordinate's in bits 16..18 and 27 (the four rotations use each bit
+// of the word once).
+constexpr int kP14PairWordPos[3] = {0, 32, 64};
 constexpr int kP14ClassPos = 96;
+
+// The pairs the GEMV multiplies with the staged activation, in summation
+// order: pair q = (kPairCoords[q][0], kPairCoords[q][1]).
+constexpr int kPairCoords[12][2] = {{0, 16}, {4, 20}, {8, 12}, {1, 17}, {5, 21}, {9, 13},
+                                    {2, 18}, {6, 22}, {10, 14}, {3, 19}, {7, 23}, {11, 15}};
+
+__host__ __device__ inline uint32_t p14_rotl(uint32_t v, int s) {
+  s &= 31;
+  return s ? (v << s) | (v >> (32 - s)) : v;
+}
+
+// Planes14 pair words of a block from each coordinate's level code (1..5) and
+// its non-negative bit (bit i of pos).
+__host__ __device__ inline void planes14_words(const uint8_t code[24], uint32_t pos,
+                                               uint32_t w[3]) {
+  w[0] = w[1] = w[2] = 0;
+  for (int q = 0; q < 12; ++q) {
+    const int a = kPairCoords[q][0], b = kPairCoords[q][1];
+    const uint32_t sel = (uint32_t)code[a] | (pos >> a & 1u) << 11 | (uint32_t)code[b] << 16 |
+                         (pos >> b & 1u) << 27;
+    w[q >> 2] |= p14_rotl(sel, 4 * (q & 3));
+  }
+}
+
+// The inverse: level codes and the non-negative mask of a block's pair words.
+__host__ __device__ inline void planes14_codes(const uint32_t w[3], uint8_t code[24],
+                                               uint32_t* pos) {
+  uint32_t p = 0;
+  for (int q = 0; q < 12; ++q) {
+    const uint32_t sel = p14_rotl(w[q >> 2], 32 - 4 * (q & 3)) & 0x08070807u;
+    const int a = kPairCoords[q][0], b = kPairCoords[q][1];
+    code[a] = (uint8_t)(sel & 7u);
+    code[b] = (uint8_t)(sel >> 16 & 7u);
+    p |= (sel >> 11 & 1u) << a | (sel >> 27 & 1u) << b;
+  }
+  *pos = p;
+}
 constexpr int kPlanes12Bytes = 12;
 constexpr int kGolay70Bytes = 9;
 constexpr int kSlot32Small = 16;     // ≤ 4 levels
@@ -65,22 +105,6 @@ struct DevClass {
 };
 constexpr int kSignByteCode = 0;
 __host__ __device__ inline int level_code(int level) { return level + 1; }
-
-// The three level-code planes and the non-negative plane of a block as the
-// four Planes14 nibble words: bit q of nibble g of w[r] is bit 4g + r of
-// plane q (the four planes transposed by nibble).
-__host__ __device__ inline void planes_to_nibbles(uint32_t p0, uint32_t p1, uint32_t p2,
-                                                  uint32_t pos, uint32_t w[4]) {
-  for (int r = 0; r < 4; ++r) {
-    uint32_t v = 0;
-    for (int g = 0; g < 6; ++g) {
-      const int i = 4 * g + r;
-      v |= ((p0 >> i & 1u) | (p1 >> i & 1u) << 1 | (p2 >> i & 1u) << 2 | (pos >> i & 1u) << 3)
-           << (4 * g);
-    }
-    w[r] = v;
-  }
-}
 static_assert(sizeof(DevClass) == 32, "device class record is 32 bytes");
 
 // Geometry shared by the expansion and the kernels: rows are grouped into

@@ -10,8 +10,8 @@
 // blocks apart, so these reads gather) and decodes it with the shared
 // format-v1 routines: a binary search over the class offsets, two or three
 // 64-bit divisions into the mixed-radix digits, colex unranking of each
-// level's positions straight into the three level-code planes, and the planes
-// sliced into the record's nibble words.  The index
+// level's positions straight into the three level-code planes, and the
+// record's pair words built from them.  The index
 // table (60 KiB) is read through the caches.  A grid-stride loop bounds the
 // grid; every thread leaves once its slots pass the end of the stream.
 
@@ -41,9 +41,8 @@ struct TranscodeArgs {
   int C, R;
 };
 
-// Record words of one block: w0 | w3[0:8) << 24, w1 | w3[8:16) << 24,
-// w2 | w3[16:24) << 24 (the nibble words of the block's planes), and the
-// 16-bit class | gain << 9 (the record's last two bytes).  Zeros for slots
+// Record words of one block: its three pair words and the 16-bit
+// class | gain << 9 (the record's last two bytes).  Zeros for slots
 // past the matrix and for codes that are not format-v1 codes.
 __device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, uint32_t w[4]) {
   w[0] = w[1] = w[2] = w[3] = 0;
@@ -63,10 +62,11 @@ __device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, 
     atomicAdd(a.bad, 1u);
     return;
   }
-  uint32_t n[4];
-  planes_to_nibbles(p[0], p[1], p[2], ~smask & 0xFFFFFFu, n);
+  uint8_t code[kDim];
 #pragma unroll
-  for (int k = 0; k < 3; ++k) w[k] = n[k] | (n[3] >> (8 * k) & 0xFFu) << 24;
+  for (int i = 0; i < kDim; ++i)
+    code[i] = (uint8_t)((p[0] >> i & 1u) | (p[1] >> i & 1u) << 1 | (p[2] >> i & 1u) << 2);
+  planes14_words(code, ~smask & 0xFFFFFFu, w);
   w[3] = (uint32_t)cls | (uint32_t)gain << 9;
 }
 
