@@ -563,7 +563,10 @@ __host__ __device__ constexpr bool has_exc() {
 // NB: batch width.  Each decoded block is multiplied with NB activations
 // (NB > 1: Planes14), in the same order as a single GEMV, so every output
 // vector is bit-identical to that activation's own GEMV.
-template <int LAYOUT, bool EVEN, int NB = 1>
+// XPER: activation blocks each thread stages through registers in the ordered
+// prologue (1 when the workgroup's threads cover every block, else 2; more
+// blocks go through the unordered loop first).
+template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ __attribute__((aligned(16))) LdsEntry ts[1024];
@@ -652,7 +655,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // (x blocks, class table, side data), then the last column group's loads,
   // then the pipeline's record loads, then the LDS writes, which wait only for
   // the older staging loads.
-  constexpr int kXPer = 2;                     // x blocks per thread held in registers
+  constexpr int kXPer = XPER;                  // x blocks per thread held in registers
   constexpr int kEPer = kExcLdsBytes / 16 / (kMaxWaves * 64), kUPer = 2;
   // rare overflow first (xblocks > kXPer·threads, or fewer threads than
   // classes): loads of unknown count here, before the ordered ones.  Only the
@@ -1118,19 +1121,28 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
          (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
 }
 
-template <int LAYOUT, bool EVEN, int NB = 1>
-static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
+template <int LAYOUT, bool EVEN, int NB, int XPER>
+static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
   if (shmem + kTableBytes > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN, NB>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB>), dim3((unsigned)a.tiles), dim3(64 * a.waves),
-                     shmem, st, a);
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER>), dim3((unsigned)a.tiles),
+                     dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
   return LEECH_OK;
 }
+
+template <int LAYOUT, bool EVEN, int NB = 1>
+static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
+  // one activation block per thread when the workgroup's threads cover them
+  if (NB > 1 || a.groups * a.C <= 64 * a.waves)
+    return launch_gemv_kernel<LAYOUT, EVEN, NB, 1>(a, shmem, st);
+  return launch_gemv_kernel<LAYOUT, EVEN, NB, 2>(a, shmem, st);
+}
+
 
 template <int LAYOUT, int NB = 1>
 static int launch_gemv(const GemvArgs& a, hipStream_t st) {
