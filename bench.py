@@ -30,6 +30,10 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published peak
 REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Cache
+# rotated arms that mix the two forms: the activation is rotated inside the
+# GEMV's prologue up to this K (each workgroup redoes the whole transform, which
+# pays while K is small), by the separate rotation kernel above it
+ROT_IN_KERNEL_MAX_K = 4096
 ARMS = ["planes14", "slot32", "planes12x", "planes12x_inline", "golay70", "golay70_inline",
         "fp16", "noweights"]
 CONFIGS = {"c1_768x1536": (768, 1536), "c2_4096x4096": (4096, 4096),
@@ -249,6 +253,20 @@ def bench_layer(args, torch, P, synth):
             P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
             m.gemv_grouped(xrot[f], rows, [cen] * len(rows), yf[f])
 
+    # the same, with each GEMV rotating its activation in its own prologue
+    def run_fused_rotk(i):
+        for f, (m, rows) in fus_r[i % reps].items():
+            m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
+
+    # in the prologue where K ≤ ROT_IN_KERNEL_MAX_K, a separate rotation above
+    def run_fused_rotmix(i):
+        for f, (m, rows) in fus_r[i % reps].items():
+            if raw[f].numel() <= ROT_IN_KERNEL_MAX_K:
+                m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
+            else:
+                P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
+                m.gemv_grouped(xrot[f], rows, [cen] * len(rows), yf[f])
+
     # outputs agree (fused rows are the separate rows, within f32 rounding)
     run_sep(0)
     run_fused(0)
@@ -257,7 +275,8 @@ def bench_layer(args, torch, P, synth):
     rel = float(((yf["qkv"] - ysep).abs().max() / ysep.abs().max()).item())
     res = {}
     for name, fn, nrep in (("separate", run_sep, reps), ("fused", run_fused, reps),
-                           ("fused_rot", run_fused_rot, reps), ("fp16", run_fp, fp_reps)):
+                           ("fused_rot", run_fused_rot, reps), ("fused_rotk", run_fused_rotk, reps),
+                           ("fused_rotmix", run_fused_rotmix, reps), ("fp16", run_fp, fp_reps)):
         steps = args.layer_steps
         g = torch.cuda.CUDAGraph()
         fn(0)
@@ -284,6 +303,8 @@ def bench_layer(args, torch, P, synth):
             "served_bytes": layer_bytes, "us_separate_7_launches": res["separate"],
             "us_fused_4_launches": res["fused"],
             "us_fused_with_rotation_8_launches": res["fused_rot"],
+            "us_fused_with_rotation_in_kernel_4_launches": res["fused_rotk"],
+            "us_fused_with_rotation_in_kernel_where_K_le_4096": res["fused_rotmix"],
             "us_fp16_7_launches": res["fp16"],
             "fusion_saves": round(1 - res["fused"] / res["separate"], 4),
             "fused_vs_fp16": round(res["fp16"] / res["fused"], 3),
@@ -409,6 +430,12 @@ def bench_step14b(args, torch, P, synth):
                 m.gemv_grouped(xrot[f], rows, [cen] * len(rows), yf[f])
         run_head()
 
+    def step_fused_rotk(_):
+        for layer in fus:
+            for f, (m, rows) in layer.items():
+                m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
+        run_head()
+
     def step_fp(_):
         for layer in fp:
             for n, w in layer.items():
@@ -419,7 +446,7 @@ def bench_step14b(args, torch, P, synth):
 
     res = {}
     for name, fn in (("separate", step_sep), ("fused", step_fused), ("fused_rot", step_fused_rot),
-                     ("fp16", step_fp)):
+                     ("fused_rotk", step_fused_rotk), ("fp16", step_fp)):
         res[name] = round(replay_us(torch, fn, 3), 1)
         log(f"[bench] 14B step {name}: {res[name]} us")
     head_us = round(replay_us(torch, lambda _: run_head(), 20), 1)
@@ -430,10 +457,12 @@ def bench_step14b(args, torch, P, synth):
             "layers": L, "planes14_bytes": L * leech_bytes, "fp16_bytes": L * fp_bytes,
             "head_bytes": head.numel() * 2,
             "us_separate_280": res["separate"], "us_fused_160": res["fused"],
-            "us_fused_with_rotation_320": res["fused_rot"], "us_fp16_280": res["fp16"],
+            "us_fused_with_rotation_320": res["fused_rot"],
+            "us_fused_with_rotation_in_kernel_160": res["fused_rotk"], "us_fp16_280": res["fp16"],
             "us_head": head_us,
             "fp16_vs_fused": round(res["fp16"] / res["fused"], 3),
             "fp16_vs_fused_with_rotation": round(res["fp16"] / res["fused_rot"], 3),
+            "fp16_vs_fused_with_rotation_in_kernel": round(res["fp16"] / res["fused_rotk"], 3),
             "leech_part_GBps_fused": round(L * leech_bytes / (leech_fused * 1e-6) / 1e9, 1),
             "transcode": transcode}
 
@@ -571,6 +600,49 @@ def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
     return res
 
 
+# GEMV shapes (rows, K) of the 8B and 14B rotation sites (q/k/v and gate/up
+# row-concatenated): the activation rotated by the separate kernel, or inside
+# the GEMV's prologue.
+ROT_SITES = [(4096, 4096), (6144, 4096), (28672, 4096), (4096, 14336),
+             (7168, 5120), (34816, 5120), (5120, 17408)]
+
+
+def bench_rotation_sites(args, torch, P, synth):
+    """µs per site: the GEMV on a pre-rotated activation, rotate_x then the
+    GEMV, and gemv_rotated (the rotation in the GEMV's prologue); each a graph
+    replay of args.layer_steps calls walking ≥ 1 GiB of weight replicas."""
+    dev = torch.device("cuda:0")
+    dcb = P.DeviceCodebook(P.Codebook(12), dev)
+    res = {}
+    for M, K in ROT_SITES:
+        inp = synth.make_gemv_inputs(M, K, seed=7, name=f"rotsite-{M}x{K}")
+        cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+        m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+        reps = max(1, math.ceil(REPLICA_BYTES / m0.desc.served_bytes))
+        mats = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0.clone(),
+                                     m0.side1.clone(), m0.scale.clone(), dcb)
+                       for _ in range(reps - 1)]
+        x = torch.from_numpy(inp.x[:K].copy()).to(dev)
+        sg = torch.from_numpy(synth.make_signs(K, seed=7, name=f"rotsite-{M}x{K}")).to(dev)
+        xr = P.rotate_x(x, sg, inp.Kpad)
+        y = torch.empty(M, dtype=torch.float32, device=dev)
+        n = args.layer_steps
+        row = {
+            "gemv_us": replay_us(torch, lambda i: mats[i % reps].gemv(xr, y), n),
+            "rotate_then_gemv_us": replay_us(
+                torch, lambda i: (P.rotate_x(x, sg, inp.Kpad, out=xr), mats[i % reps].gemv(xr, y)), n),
+            "gemv_rotated_us": replay_us(
+                torch, lambda i: mats[i % reps].gemv_rotated(x, sg, y=y), n),
+        }
+        row = {k: round(v, 2) for k, v in row.items()}
+        row["lane_cols"] = m0.desc.lane_cols
+        res[f"{M}x{K}"] = row
+        log(f"[bench] rotation site {M}x{K}: {row}")
+        del mats, m0
+        torch.cuda.empty_cache()
+    return res
+
+
 def measured_traffic(config):
     """HBM bytes per launch of the Planes14 GEMV from the committed counter
     runs (FETCH_SIZE + WRITE_SIZE, each scaled by a known-size copy), or None
@@ -685,6 +757,7 @@ def main():
         torch.cuda.synchronize()
         layer = bench_layer(args, torch, P, synth)
         layer["rotation"] = bench_rotation(args, torch, P, synth)
+        layer["rotation_sites"] = bench_rotation_sites(args, torch, P, synth)
     step14b = None
     if not args.no_step14b:
         for a in arms.values():

@@ -292,6 +292,25 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
 enum { LEECH_EXC_HOISTED = 0, LEECH_EXC_INLINE = 1 };
 int leech_set_exception_mode(int mode);
 
+/* GEMV behind the activation rotation in one launch (§2.3: the activation is
+ * rotated before the matvec; §6: every consumer rotates): y = W · R(x), where
+ * R is leech_rotate_x's blockwise Walsh–Hadamard rotation of the raw binary16
+ * activation d_x [K] with the signs d_signs [K] (NULL: all +1).  Each
+ * workgroup rotates the activation in LDS while its first weight loads are in
+ * flight; the result is bit-identical to leech_rotate_x(K, Kpad, d_x,
+ * d_signs, xr) followed by leech_gemv_grouped(…, xr, d_y).  Row groups and
+ * centroids as leech_gemv_grouped (n_groups = 1 for a plain GEMV).  Serves
+ * LEECH_PLANES14 (LEECH_E_LAYOUT otherwise); needs 0 < K ≤ Kpad, K a multiple
+ * of 8, the power-of-two factor of K at most 32768, K at most 40 × the
+ * workgroup's threads (20480 for matrices of 512 or more rows) and the
+ * rotation buffer within LDS (LEECH_E_SHAPE otherwise); d_x 16-byte and
+ * d_signs 8-byte aligned. */
+int leech_gemv_rotated(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                       const void* d_side1, const void* d_class_table, const void* d_codewords,
+                       const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
+                       const float* group_centroids, int64_t K, const uint16_t* d_x,
+                       const int8_t* d_signs, float* d_y, void* stream);
+
 /* Verification decode on the device with the GEMV's own decoders: z int8
  * [M·nb][24], class_id [M·nb], gain_bit [M·nb], row-major (r, j).  Any output
  * may be NULL. */

@@ -152,6 +152,30 @@ class LeechMatrix:
                           group_centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
         return y
 
+    def gemv_rotated(self, x, signs=None, group_rows=None, group_centroids=((1.0, 1.0),), y=None,
+                     stream=None):
+        """y = W · R(x) in one launch: x the raw fp16 activation [K] (K ≤ Kpad,
+        a multiple of 8), signs int8 ±1 [K] or None; R is rotate_x's rotation,
+        done by each workgroup in LDS.  Row groups as gemv_grouped (None: one
+        group of all rows)."""
+        torch = _torch()
+        if x.dtype != torch.float16 or x.dim() != 1 or not x.is_contiguous():
+            raise ValueError("x must be a contiguous 1-D fp16 tensor")
+        K = x.numel()
+        if signs is not None and (signs.dtype != torch.int8 or signs.numel() != K
+                                  or not signs.is_contiguous()):
+            raise ValueError("signs must be a contiguous int8 tensor of length K")
+        if y is None:
+            y = torch.empty(self.M, dtype=torch.float32, device=x.device)
+        rows = [self.M] if group_rows is None else group_rows
+        m, s0, s1 = self._ptrs()
+        _lib.gemv_rotated(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
+                          self.dcb.golay_gen.data_ptr(), self.scale.data_ptr(), rows,
+                          group_centroids, K, x.data_ptr(),
+                          signs.data_ptr() if signs is not None else 0, y.data_ptr(),
+                          _stream(stream))
+        return y
+
     def decode(self, stream=None):
         """Device decode: (z int8 [M, nb, 24], class_id int16 [M, nb], gain uint8 [M, nb])."""
         torch = _torch()

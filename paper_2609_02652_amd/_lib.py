@@ -28,7 +28,8 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_host_decode_layout", "leech_gemv", "leech_gemv_grouped", "leech_decode_blocks",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
-           "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch"]
+           "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch",
+           "leech_gemv_rotated"]
 
 
 class LeechError(RuntimeError):
@@ -81,6 +82,8 @@ def _load() -> C.CDLL:
         "leech_set_exception_mode": (I, [I]),
         "leech_gemv_batch": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, I, P, I64, P, I64,
                                  P]),
+        "leech_gemv_rotated": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, I, P, P, I64, P, P,
+                                   P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -244,6 +247,17 @@ def gemv_batch(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, ce
     check(lib.leech_gemv_batch(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
                                d_codewords or None, d_scale, C.cast(cen, C.c_void_p), batch, d_X,
                                ldx, d_Y, ldy, stream or None))
+
+
+def gemv_rotated(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, group_rows,
+                 group_centroids, K, d_x, d_signs, d_y, stream=0):
+    n = len(group_rows)
+    rows = (C.c_int64 * max(n, 1))(*[int(r) for r in group_rows])
+    cen = (C.c_float * max(2 * n, 2))(*[float(c) for pair in group_centroids for c in pair])
+    check(lib.leech_gemv_rotated(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
+                                 d_codewords or None, d_scale, n, C.cast(rows, C.c_void_p),
+                                 C.cast(cen, C.c_void_p), K, d_x, d_signs or None, d_y,
+                                 stream or None))
 
 
 MAX_GROUPS = 8

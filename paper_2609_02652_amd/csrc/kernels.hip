@@ -55,6 +55,8 @@ typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
 typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
 typedef uint32_t u32x4a __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2a __attribute__((ext_vector_type(2)));
+typedef float f32x4a __attribute__((ext_vector_type(4)));
 
 constexpr int kNoWeights = 99;   // layout id of the no-weights control
 #ifndef LEECH_PREFETCH
@@ -104,6 +106,13 @@ struct GemvArgs {
   // b < nbatch (≤ the kernel's batch width)
   int64_t ldx, ldy;
   int nbatch;
+  // rotated launches: the activation is rotated in the prologue from the raw
+  // binary16 xraw [K] and the ±1 signs (NULL: all +1), blocks of 2^rot_k
+  const uint16_t* xraw;
+  const int8_t* signs;
+  int64_t K;
+  int rot_k;
+  float rot_norm;
 };
 
 // Where side data comes from: global memory (verification decode, and the
@@ -271,7 +280,7 @@ __device__ __forceinline__ void golay70_core(uint32_t c0, uint32_t c1, uint32_t 
 }
 
 // Coordinates of pair k of h[] (and of the staged x pairs).
-__device__ __forceinline__ void pair_coords(int k, int& c0, int& c1) {
+__host__ __device__ constexpr void pair_coords(int k, int& c0, int& c1) {
   const int r = k / 3, m = k % 3;
   c0 = m == 0 ? r : (m == 1 ? 4 + r : 8 + r);
   c1 = m == 0 ? 16 + r : (m == 1 ? 20 + r : 12 + r);
@@ -546,6 +555,174 @@ __device__ __forceinline__ float dot12(const uint32_t h[12], const uint32_t xw[1
   return s;
 }
 
+// ------------------------------------------------------- fused rotation
+// The activation rotation (blockwise Walsh–Hadamard, §2.3, §6) done by each
+// GEMV workgroup in its prologue, while its first record loads are in flight:
+// a thread holds up to kRotG groups of 8 consecutive coordinates (loaded
+// first), applies the butterflies of index bits 0..2 in registers, the
+// workgroup applies bits 3.. in radix-8 passes over an f32 copy in LDS, and a
+// last pass scales by 2^(-k/2), rounds to binary16 (the product is rounded to
+// f32 first) and stages the blocks in pair order.  Stage order and arithmetic
+// are leech_rotate_x's, so the staged activation equals that call's output.
+constexpr int kRotG = 5;      // groups of 8 coordinates per thread: K ≤ 40 · threads
+
+__device__ __forceinline__ int rot_pad(int i) { return i + ((i >> 6) << 3); }
+
+template <int E>
+__device__ __forceinline__ void rot_butterflies(float* v) {
+#pragma unroll
+  for (int st = 1; st < E; st <<= 1)
+#pragma unroll
+    for (int t = 0; t < E; ++t)
+      if (!(t & st)) {
+        const float x = v[t], y = v[t | st];
+        v[t] = x + y;
+        v[t | st] = x - y;
+      }
+}
+
+// One radix-2^BITS pass over index bits [LO, LO + BITS) of the K coordinates.
+// The pass's bits are clear in b0 and the others clear in t << LO, so
+// rot_pad(b0 + (t << LO)) = rot_pad(b0) + rot_pad(t << LO): one address per
+// group and constant offsets.
+template <int LO, int BITS>
+__device__ __forceinline__ void rot_pass(float* rb, int K, int tid, int nthr) {
+  constexpr int E = 1 << BITS;
+  const int ngrp = K >> BITS;
+  for (int grp = tid; grp < ngrp; grp += nthr) {
+    float* base = rb + rot_pad(((grp >> LO) << (LO + BITS)) | (grp & ((1 << LO) - 1)));
+    float v[E];
+#pragma unroll
+    for (int t = 0; t < E; ++t) v[t] = base[rot_pad(t << LO)];
+    rot_butterflies<E>(v);
+#pragma unroll
+    for (int t = 0; t < E; ++t) base[rot_pad(t << LO)] = v[t];
+  }
+}
+
+// Passes over index bits 3..k − 1, each after a barrier: (LO, BITS) pairs in
+// increasing bit order.
+template <int LO, int BITS, int... REST>
+__device__ __forceinline__ void rot_passes(float* rb, int K, int tid, int nthr) {
+  __syncthreads();
+  rot_pass<LO, BITS>(rb, K, tid, nthr);
+  if constexpr (sizeof...(REST) > 0) rot_passes<REST...>(rb, K, tid, nthr);
+}
+
+// The fewest passes of at most 4 bits each, the bits spread evenly over
+// them: a pass costs a barrier and a round trip through LDS per group, so a
+// split such as 3 + 3 + 1 (k = 10) would pay a third pass, and one with
+// K / 2 groups, for a single bit.
+__device__ __forceinline__ void rot_lds_stages(float* rb, int K, int k, int tid, int nthr) {
+  switch (k) {
+    case 4: rot_passes<3, 1>(rb, K, tid, nthr); break;
+    case 5: rot_passes<3, 2>(rb, K, tid, nthr); break;
+    case 6: rot_passes<3, 3>(rb, K, tid, nthr); break;
+    case 7: rot_passes<3, 4>(rb, K, tid, nthr); break;
+    case 8: rot_passes<3, 3, 6, 2>(rb, K, tid, nthr); break;
+    case 9: rot_passes<3, 3, 6, 3>(rb, K, tid, nthr); break;
+    case 10: rot_passes<3, 4, 7, 3>(rb, K, tid, nthr); break;
+    case 11: rot_passes<3, 4, 7, 4>(rb, K, tid, nthr); break;
+    case 12: rot_passes<3, 3, 6, 3, 9, 3>(rb, K, tid, nthr); break;
+    case 13: rot_passes<3, 4, 7, 3, 10, 3>(rb, K, tid, nthr); break;
+    case 14: rot_passes<3, 4, 7, 4, 11, 3>(rb, K, tid, nthr); break;
+    case 15: rot_passes<3, 4, 7, 4, 11, 4>(rb, K, tid, nthr); break;
+    default: break;     // k ≤ 3: every stage ran in registers
+  }
+}
+
+// Half-word position (2·pair + half) of coordinate c of a block in pair
+// order: the inverse of pair_coords.
+__host__ __device__ constexpr int pair_half_of(int c) {
+  return c < 4 ? 6 * c : c < 8 ? 6 * (c - 4) + 2 : c < 12 ? 6 * (c - 8) + 4
+       : c < 16 ? 6 * (c - 12) + 5 : c < 20 ? 6 * (c - 16) + 1 : 6 * (c - 20) + 3;
+}
+
+__host__ __device__ constexpr bool pair_half_inverts() {
+  for (int k = 0; k < 12; ++k) {
+    int c0 = 0, c1 = 0;
+    pair_coords(k, c0, c1);
+    if (pair_half_of(c0) != 2 * k || pair_half_of(c1) != 2 * k + 1) return false;
+  }
+  return true;
+}
+static_assert(pair_half_inverts(), "pair_half_of inverts pair_coords");
+
+__device__ void rotate_activation(const GemvArgs& a, const u32x4a* rx, const u32x2a* rsg,
+                                  float* rb, uint32_t* xs, int xblocks, int tid, int nthr) {
+  const int k = a.rot_k;
+  const int K = (int)a.K;
+#pragma unroll
+  for (int q = 0; q < kRotG; ++q) {
+    const int e0 = 8 * (tid + q * nthr);
+    if (e0 < K) {
+      float v[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float f = (float)__builtin_bit_cast(_Float16, (uint16_t)(rx[q][t >> 1] >> (16 * (t & 1))));
+        // bit 7 of the sign byte set means −1: it becomes the f32 sign bit
+        const uint32_t neg = (rsg[q][t >> 2] >> (8 * (t & 3)) << 24) & 0x80000000u;
+        v[t] = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f) ^ neg);
+      }
+      if (k >= 3) {
+        rot_butterflies<8>(v);
+      } else if (k == 2) {
+        rot_butterflies<4>(v);
+        rot_butterflies<4>(v + 4);
+      } else if (k == 1) {
+#pragma unroll
+        for (int t = 0; t < 8; t += 2) rot_butterflies<2>(v + t);
+      }
+      float* d = rb + rot_pad(e0);
+      *reinterpret_cast<f32x4a*>(d) = f32x4a{v[0], v[1], v[2], v[3]};
+      *reinterpret_cast<f32x4a*>(d + 4) = f32x4a{v[4], v[5], v[6], v[7]};
+    }
+  }
+  // the entry point admits k ≤ 15
+  rot_lds_stages(rb, K, k, tid, nthr);
+  __syncthreads();
+  // scale, round (to f32, then binary16) and store each coordinate at its
+  // place in its block's pair order; zero past K up to the staged blocks' end.
+  // A group of 8 is a third of a block: coordinates 0..7 and 16..23 fill the
+  // low and the high halves of the same eight words, 8..15 four whole words.
+  auto rounded = [&](int e0, uint32_t* h) {
+    if (e0 < K) {
+      const float* d = rb + rot_pad(e0);
+      const f32x4a lo4 = *reinterpret_cast<const f32x4a*>(d);
+      const f32x4a hi4 = *reinterpret_cast<const f32x4a*>(d + 4);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        float r = (t < 4 ? lo4[t] : hi4[t - 4]) * a.rot_norm;
+        asm("" : "+v"(r));
+        h[t] = __builtin_bit_cast(uint16_t, (_Float16)r);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) h[t] = 0;
+    }
+  };
+  auto place = [&](int e0, const uint32_t* h) {
+    const int g = e0 >> 3, j = g / 3, third = g - 3 * j;
+    uint32_t* blk = xs + 12 * j;
+    uint16_t* half = reinterpret_cast<uint16_t*>(blk);
+    if (third == 1) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) blk[pair_half_of(8 + t) >> 1] = h[t] | h[t + 4] << 16;
+    } else if (third == 0) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) half[pair_half_of(t)] = (uint16_t)h[t];
+    } else {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) half[pair_half_of(16 + t)] = (uint16_t)h[t];
+    }
+  };
+  for (int e0 = 8 * tid; e0 < 24 * xblocks; e0 += 8 * nthr) {
+    uint32_t h[8];
+    rounded(e0, h);
+    place(e0, h);
+  }
+}
+
 // ------------------------------------------------------------------- GEMV
 // LDS: the class table in a static array (entry e at byte e·16 of it, so a
 // decoded field is its own address), then, dynamically sized, x for groups·C
@@ -566,7 +743,11 @@ __host__ __device__ constexpr bool has_exc() {
 // XPER: activation blocks each thread stages through registers in the ordered
 // prologue (1 when the workgroup's threads cover every block, else 2; more
 // blocks go through the unordered loop first).
-template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2>
+// ROT: the activation arrives unrotated and the workgroup rotates it itself
+// (Planes14, NB = 1): blockwise Walsh–Hadamard with the caller's signs, the
+// stages in the order and arithmetic of leech_rotate_x, so the staged binary16
+// activation is bit-identical to that call's output.
+template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ __attribute__((aligned(16))) LdsEntry ts[1024];
@@ -588,7 +769,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if constexpr (kExc) p += kExcLdsBytes;
   float* pre = (float*)p;                                               // kPreFloats
   if constexpr (kExc) p += kPreFloats * 4;
-  float* red = (float*)p;                                               // waves × 64
+  float* red = (float*)p;                                          // NB × waves × 64
+  float* rb = red + NB * waves * 64;                               // ROT: rotation buffer
 
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int tile = (int)blockIdx.x;
@@ -663,6 +845,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // gain entries of a class from one read of its table record.
   // (a batched launch stages all its activations here: vector b's blocks
   // follow vector b − 1's, zero past nb and for vectors past nbatch)
+  if constexpr (!ROT)
   for (int j = NB == 1 ? tid + kXPer * nthr : tid; j < NB * xblocks; j += nthr) {
     const int b = NB == 1 ? 0 : j / xblocks, jb = j - b * xblocks;
     if (jb < nb && b < a.nbatch) {
@@ -699,10 +882,25 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // (no class) to stage loads through the null descriptor, and lanes past nb
   // read zeros, which is the padding past the last column
   const __amdgpu_buffer_rsrc_t rs_x = make_rsrc(a.x, (uint64_t)nb * 48);
+  // ROT: the raw activation and its signs, eight coordinates per load
+  u32x4a rx[kRotG];
+  u32x2a rsg[kRotG];
+  if constexpr (ROT) {
+    const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.xraw, (uint64_t)a.K * 2);
+    const __amdgpu_buffer_rsrc_t rsn = a.signs ? make_rsrc(a.signs, (uint64_t)a.K) : null_rsrc();
+#pragma unroll
+    for (int q = 0; q < kRotG; ++q) {
+      const bool live = (int64_t)(q * nthr + wave * 64) * 8 < a.K;
+      rx[q] = __builtin_amdgcn_raw_buffer_load_b128(live ? rr : null_rsrc(), (tid + q * nthr) * 16,
+                                                    0, 0);
+      rsg[q] = __builtin_amdgcn_raw_buffer_load_b64(live ? rsn : null_rsrc(), (tid + q * nthr) * 8,
+                                                    0, 0);
+    }
+  }
   XBlock xr[kXPer];
 #pragma unroll
   for (int q = 0; q < kXPer; ++q) {
-    const bool live = NB == 1 && q * nthr + wave * 64 < nb;
+    const bool live = NB == 1 && !ROT && q * nthr + wave * 64 < nb;
     const int off = (tid + q * nthr) * 48;
     const __amdgpu_buffer_rsrc_t r = live ? rs_x : null_rsrc();
     xr[q].v0 = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
@@ -756,13 +954,14 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     pf[d] = load_unit<LAYOUT, EVEN>(a, t, d < units, Lp, min(wave + d * waves, g_stand), gside);
     __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
   }
-  if constexpr (NB == 1) {
+  if constexpr (NB == 1 && !ROT) {
 #pragma unroll
     for (int q = 0; q < kXPer; ++q) {
       const int j = tid + q * nthr;
       if (j < xblocks) store_x_block(xr[q], xs + 12 * j);
     }
   }
+  if constexpr (ROT) rotate_activation(a, rx, rsg, rb, xs, xblocks, tid, nthr);
   if constexpr (kW) {
     if (tid < kBallClasses) {
       LdsEntry e;
@@ -1121,14 +1320,14 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
          (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
 }
 
-template <int LAYOUT, bool EVEN, int NB, int XPER>
+template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false>
 static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
   if (shmem + kTableBytes > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER>,
+    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER>), dim3((unsigned)a.tiles),
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT>), dim3((unsigned)a.tiles),
                      dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
@@ -1152,6 +1351,21 @@ static int launch_gemv(const GemvArgs& a, hipStream_t st) {
   if (LAYOUT == kNoWeights || even_bases(a, LAYOUT))
     return launch_gemv_as<LAYOUT, true, NB>(a, shmem, st);
   return launch_gemv_as<LAYOUT, false, NB>(a, shmem, st);
+}
+
+// Rotated launches (Planes14): the LDS of a plain launch plus the f32
+// rotation buffer.
+static size_t rot_lds_bytes(const GemvArgs& a) {
+  return gemv_lds_bytes<LEECH_PLANES14>(a) + ((size_t)a.K + (size_t)(a.K >> 6) * 8 + 16) * 4;
+}
+
+static int launch_gemv_rotated(const GemvArgs& a, hipStream_t st) {
+  const size_t shmem = rot_lds_bytes(a);
+  if (shmem + kTableBytes > 160 * 1024)
+    return set_error(LEECH_E_SHAPE, "K too large for the LDS-staged rotation");
+  if (even_bases(a, LEECH_PLANES14))
+    return launch_gemv_kernel<LEECH_PLANES14, true, 1, 1, true>(a, shmem, st);
+  return launch_gemv_kernel<LEECH_PLANES14, false, 1, 1, true>(a, shmem, st);
 }
 
 // Batch width of the next chunk of a batched launch: 2, 4 or 8 (the next
@@ -1273,19 +1487,15 @@ int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const vo
   return LEECH_OK;
 }
 
-int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
-                       const void* d_side1, const void* d_class_table, const void* d_codewords,
-                       const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
-                       const float* group_centroids, const uint16_t* d_x, float* d_y,
-                       void* stream) {
-  clear_error();
+}  // extern "C"
+
+namespace leech {
+// Row groups of a grouped launch, validated into the launch arguments.
+static int set_groups(const leech_layout_desc* desc, int n_groups, const int64_t* group_rows,
+                      const float* group_centroids, GemvArgs& a) {
   if (!group_rows || !group_centroids) return set_error(LEECH_E_ARG, "NULL argument");
   if (n_groups < 1 || n_groups > LEECH_MAX_GROUPS)
     return set_error(LEECH_E_ARG, "n_groups must be 1.." + std::to_string(LEECH_MAX_GROUPS));
-  GemvArgs a;
-  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_x,
-                      d_y, &a);
-  if (rc) return rc;
   int64_t end = 0;
   for (int g = 0; g < n_groups; ++g) {
     if (group_rows[g] <= 0) return set_error(LEECH_E_SHAPE, "every group needs rows");
@@ -1303,6 +1513,58 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
   a.ngroups = n_groups;
   a.cen0 = a.grp_cen[0][0];
   a.cen1 = a.grp_cen[0][1];
+  return LEECH_OK;
+}
+}  // namespace leech
+
+extern "C" {
+
+int leech_gemv_rotated(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                       const void* d_side1, const void* d_class_table, const void* d_codewords,
+                       const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
+                       const float* group_centroids, int64_t K, const uint16_t* d_x,
+                       const int8_t* d_signs, float* d_y, void* stream) {
+  clear_error();
+  GemvArgs a;
+  // d_x stands in for the staged activation in the shared checks (alignment)
+  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_x,
+                      d_y, &a);
+  if (rc) return rc;
+  if (desc->layout != LEECH_PLANES14)
+    return set_error(LEECH_E_LAYOUT, "rotated GEMVs serve the PLANES14 layout");
+  rc = set_groups(desc, n_groups, group_rows, group_centroids, a);
+  if (rc) return rc;
+  if (K <= 0 || K > desc->Kpad || K % 8)
+    return set_error(LEECH_E_SHAPE, "need 0 < K <= Kpad and K a multiple of 8");
+  const int64_t n = K & -K;
+  int k = 0;
+  while ((int64_t)1 << k < n) ++k;
+  if (k > 15) return set_error(LEECH_E_SHAPE, "power-of-two factor of K above 32768");
+  if (K > (int64_t)8 * kRotG * 64 * a.waves)
+    return set_error(LEECH_E_SHAPE, "K too large for a fused rotation at this shape");
+  if ((uintptr_t)d_signs & 7) return set_error(LEECH_E_ARG, "misaligned device pointer");
+  a.x = nullptr;
+  a.xraw = d_x;
+  a.signs = d_signs;
+  a.K = K;
+  a.rot_k = k;
+  a.rot_norm = (float)(1.0 / std::sqrt((double)n));
+  return launch_gemv_rotated(a, (hipStream_t)stream);
+}
+
+int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                       const void* d_side1, const void* d_class_table, const void* d_codewords,
+                       const uint16_t* d_scale, int n_groups, const int64_t* group_rows,
+                       const float* group_centroids, const uint16_t* d_x, float* d_y,
+                       void* stream) {
+  clear_error();
+  if (!group_rows || !group_centroids) return set_error(LEECH_E_ARG, "NULL argument");
+  GemvArgs a;
+  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_x,
+                      d_y, &a);
+  if (rc) return rc;
+  rc = set_groups(desc, n_groups, group_rows, group_centroids, a);
+  if (rc) return rc;
   return gemv_dispatch(desc, a, (hipStream_t)stream);
 }
 

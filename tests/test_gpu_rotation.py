@@ -109,3 +109,54 @@ def test_rotation_feeds_gemv(dev):
     e = D.errors(y, D.gemv64(W, xr_h), W, xr_h)
     say(f"    rotated GEMV errors {e}")
     assert e["max_norm_err"] <= 2e-3 and e["max_abs_err"] <= 1e-5
+
+
+# ------------------------------------------------ rotation fused into the GEMV
+FUSED = [(768, 1536, True), (4096, 4096, True), (1024, 14336, True), (5120, 17408, True),
+         (64, 408, True), (3, 24, False), (257, 1000, False)]
+
+
+@pytest.mark.parametrize("M,K,with_signs", FUSED)
+def test_fused_rotation_equals_rotate_then_gemv(dev, M, K, with_signs):
+    """leech_gemv_rotated gives the bits of leech_rotate_x followed by the GEMV."""
+    say(f"[fused rotation] {M}x{K} signs={with_signs}")
+    inp = synth.make_gemv_inputs(M, K, seed=M + K, name="fused-rot")
+    cb = P.Codebook(12)
+    dcb = P.DeviceCodebook(cb, dev)
+    cls, sm, lv = cb.fields_from_points(inp.z)
+    mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    x = torch.from_numpy(inp.x[:K].copy()).to(dev)
+    s = torch.from_numpy(synth.make_signs(K, seed=K, name="fused-rot")).to(dev) if with_signs else None
+    cen = (0.75, 1.25)
+    y_fused = mat.gemv_rotated(x, s, group_centroids=(cen,)).cpu().numpy()
+    xr = P.rotate_x(x, s, inp.Kpad)
+    y_two = mat.gemv(xr, centroids=cen).cpu().numpy()
+    assert np.array_equal(y_fused.view(np.uint32), y_two.view(np.uint32))
+    # and against the oracle: W · R(x) with R from the oracle's rotation
+    if M <= 1024:
+        xr64 = R.rotate_padded64(inp.x[:K], s.cpu().numpy() if with_signs else np.ones(K), inp.Kpad)
+        xr16 = xr64.astype(np.float16)
+        W = D.weights64_from_points(inp.z, inp.gain, inp.scale, cen)
+        e = D.errors(y_fused, D.gemv64(W, xr16), W, xr16)
+        assert e["max_norm_err"] <= 2e-3, e
+
+
+def test_fused_rotation_grouped(dev):
+    """q/k/v fused and rotated in one launch, bit-identical to rotate + grouped."""
+    parts = [(256, 1536), (64, 1536), (64, 1536)]
+    ins = [synth.make_gemv_inputs(M, K, seed=40 + i, name=f"frg{i}") for i, (M, K) in enumerate(parts)]
+    z = np.concatenate([i.z for i in ins])
+    gain = np.concatenate([i.gain for i in ins])
+    scale = np.concatenate([i.scale for i in ins])
+    cb = P.Codebook(12)
+    dcb = P.DeviceCodebook(cb, dev)
+    cls, sm, lv = cb.fields_from_points(z)
+    mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, gain, sm, lv, scale, dev)
+    K = 1536
+    x = torch.from_numpy(ins[0].x[:K].copy()).to(dev)
+    s = torch.from_numpy(synth.make_signs(K, seed=4, name="frg")).to(dev)
+    cens = [(0.75, 1.25), (0.9, 1.1), (1.3, 0.6)]
+    rows = [M for M, _ in parts]
+    y1 = mat.gemv_rotated(x, s, rows, cens).cpu().numpy()
+    y2 = mat.gemv_grouped(P.rotate_x(x, s, mat.Kpad), rows, cens).cpu().numpy()
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))

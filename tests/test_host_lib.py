@@ -239,6 +239,28 @@ def test_batch_gemv_validates_before_launch():
         assert e.value.code == code, (layout, batch, ldx, ldy, _lib.lib.leech_last_error())
 
 
+def test_rotated_gemv_validates_before_launch():
+    d = P.LayoutDesc()
+    d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 128, 48, 2
+    d.lane_cols = 16
+    fake = 256
+    cases = [
+        (P.PLANES14, 0, -3),          # K = 0
+        (P.PLANES14, 72, -3),         # K above Kpad
+        (P.PLANES14, 44, -3),         # K not a multiple of 8
+        (P.GOLAY70, 48, -2),          # rotated launches serve Planes14
+    ]
+    for layout, K, code in cases:
+        d.layout = layout
+        with pytest.raises(P.LeechError) as e:
+            _lib.gemv_rotated(d, fake, 0, 0, fake, fake, fake, [128], [(1, 1)], K, fake, 0, fake)
+        assert e.value.code == code, (layout, K, _lib.lib.leech_last_error())
+    d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 8, 24 * 1000, 1000
+    with pytest.raises(P.LeechError) as e:        # K above 40 × 512 threads
+        _lib.gemv_rotated(d, fake, 0, 0, fake, fake, fake, [8], [(1, 1)], 24 * 1000, fake, 0, fake)
+    assert e.value.code == -3
+
+
 def test_rotate_validates_before_launch():
     fake = 256
     for K, Kpad, code in ((0, 24, -3), (48, 24, -3), (65536, 65544, -3)):
