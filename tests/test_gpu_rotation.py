@@ -112,8 +112,13 @@ def test_rotation_feeds_gemv(dev):
 
 
 # ------------------------------------------------ rotation fused into the GEMV
+# k = log2 of the largest power of two dividing K: 9, 12, 11, 10, 3, 3, 3, then
+# one case for each other k the fused path admits (4..8, 13, 14), since each
+# k has its own schedule of LDS passes
 FUSED = [(768, 1536, True), (4096, 4096, True), (1024, 14336, True), (5120, 17408, True),
-         (64, 408, True), (3, 24, False), (257, 1000, False)]
+         (64, 408, True), (3, 24, False), (257, 1000, False),
+         (256, 48, True), (256, 96, True), (256, 320, True), (256, 384, True), (200, 768, True),
+         (512, 8192, True), (256, 16384, True)]
 
 
 @pytest.mark.parametrize("M,K,with_signs", FUSED)
