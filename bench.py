@@ -147,7 +147,55 @@ def build_arms(args, torch, P, synth):
         log(f"[bench] fp16: {served} bytes/GEMV, {reps} replicas")
     if "noweights" in wanted:
         arms["noweights"] = Arm("noweights", [lambda: P.noweights_ctrl(base_desc, x, y)], 0)
-    return inp, arms
+    return inp, arms, y
+
+
+def verify_arms(torch, inp, arms, y):
+    """Every arm's output, before any timing (as §3.1 checks every arm first):
+    each replica of each layout gives the Planes14 output bit for bit (all
+    layouts sum in one order); the FP16 control agrees within
+    max_r |Δy_r| / (‖W_r‖·‖x‖) ≤ 2e-3, with ‖W_r‖ from the block scales (each
+    block direction has unit norm, centroids 1); the no-weights control writes
+    one value, Σx, on every row."""
+    import numpy as np
+    res = {"replicas_checked": 0}
+
+    def out(launch):
+        launch()
+        torch.cuda.synchronize()
+        return y.clone()
+
+    ref = out(arms["planes14"].launchers[0])
+    if not bool(torch.isfinite(ref).all()):
+        sys.exit("verification failed: planes14 output is not finite")
+    same = []
+    for name, arm in arms.items():
+        if name in ("fp16", "noweights"):
+            continue
+        for i, launch in enumerate(arm.launchers):
+            if not torch.equal(out(launch).view(torch.int32), ref.view(torch.int32)):
+                sys.exit(f"verification failed: {name} replica {i} differs from planes14")
+            res["replicas_checked"] += 1
+        same.append(name)
+    res["bit_identical_to_planes14"] = same
+    if "fp16" in arms:
+        w_norm = np.sqrt((inp.scale.astype(np.float64) ** 2).sum(axis=1))
+        x_norm = float(np.linalg.norm(inp.x.astype(np.float64)))
+        worst = 0.0
+        for i, launch in enumerate(arms["fp16"].launchers):
+            d = (out(launch) - ref).abs().double().cpu().numpy()
+            worst = max(worst, float((d / (w_norm * x_norm)).max()))
+            res["replicas_checked"] += 1
+        if not worst <= 2e-3:
+            sys.exit(f"verification failed: fp16 control differs by {worst:.3g} (normalised)")
+        res["fp16_max_normalised_diff"] = worst
+    if "noweights" in arms:
+        yn = out(arms["noweights"].launchers[0])
+        if not (bool(torch.isfinite(yn).all()) and bool((yn == yn[0]).all())):
+            sys.exit("verification failed: no-weights control rows differ")
+        res["noweights_rows_equal"] = True
+    log(f"[bench] verified before timing: {res}")
+    return res
 
 
 def time_arm(torch, arm, steps):
@@ -710,8 +758,9 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] copy reference: 5 × {n} bytes read and written")
         del src, dst
-    inp, arms = build_arms(args, torch, P, synth)
+    inp, arms, y_arms = build_arms(args, torch, P, synth)
     main_arm = arms["planes14"]
+    verified = verify_arms(torch, inp, arms, y_arms)
 
     # warmup every arm (eager, then its graphs), then the contract's timed
     # region: K Planes14 GEMVs
@@ -794,6 +843,7 @@ def main():
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config)},
         "arms": table,
+        "verified": verified,
         "batch": batch,
         "layer_8b": layer,
         "step_14b": step14b,
