@@ -737,6 +737,14 @@ __host__ __device__ constexpr bool has_exc() {
   return LAYOUT == LEECH_PLANES12X || LAYOUT == LEECH_GOLAY70;
 }
 
+// A batched launch (NB > 1) keeps its cross-wave reduction in the activation
+// area, which the loop no longer reads once every wave has finished, when
+// each activation's share of it holds that activation's partial sums (64 per
+// wave); a single GEMV keeps a separate buffer.
+__host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int waves) {
+  return nb_vectors > 1 && xblocks * 48 >= waves * 64 * 4;
+}
+
 // NB: batch width.  Each decoded block is multiplied with NB activations
 // (NB > 1: Planes14), in the same order as a single GEMV, so every output
 // vector is bit-identical to that activation's own GEMV.
@@ -769,8 +777,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if constexpr (kExc) p += kExcLdsBytes;
   float* pre = (float*)p;                                               // kPreFloats
   if constexpr (kExc) p += kPreFloats * 4;
-  float* red = (float*)p;                                          // NB × waves × 64
-  float* rb = red + NB * waves * 64;                               // ROT: rotation buffer
+  const bool red_x = red_in_x(NB, xblocks, waves);
+  float* red = red_x ? (float*)smem : (float*)p;                   // NB × waves × 64
+  float* rb = (float*)p + NB * waves * 64;                         // ROT (NB = 1): rotation buffer
 
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int tile = (int)blockIdx.x;
@@ -1145,6 +1154,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // the last column group, by the wave next in turn; its lanes past the last
   // column read zero x and add exactly zero
   if (wave == w_last) process(plast, gf, Ll);
+  if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     float v = acc[b];
@@ -1313,11 +1323,11 @@ static bool even_bases(const GemvArgs& a, int layout) {
 
 template <int LAYOUT, int NB = 1>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
-  return (size_t)NB * a.groups * a.C * 48 + (size_t)(NB - 1) * a.waves * 64 * 4 +
-         (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
+  const size_t red = red_in_x(NB, a.groups * a.C, a.waves) ? 0 : (size_t)NB * a.waves * 64 * 4;
+  return (size_t)NB * a.groups * a.C * 48 + (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
          (has_exc<LAYOUT>() ? kExcLdsBytes : 0) +
-         (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + (size_t)a.waves * 64 * 4;
+         (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + red;
 }
 
 template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false>
@@ -1374,10 +1384,12 @@ static int launch_gemv_rotated(const GemvArgs& a, hipStream_t st) {
 // a single vector left, or when not even two fit.
 static int batch_width(const GemvArgs& a, int left) {
   if (left <= 1) return 1;
-  const size_t one = gemv_lds_bytes<LEECH_PLANES14>(a);
-  const size_t per = (size_t)a.groups * a.C * 48 + (size_t)a.waves * 64 * 4;
-  for (int w = left > 4 ? 8 : left > 2 ? 4 : 2; w >= 2; w >>= 1)
-    if (one + (size_t)(w - 1) * per + kTableBytes <= 160 * 1024) return w;
+  for (int w = left > 4 ? 8 : left > 2 ? 4 : 2; w >= 2; w >>= 1) {
+    const size_t need = w == 8   ? gemv_lds_bytes<LEECH_PLANES14, 8>(a)
+                        : w == 4 ? gemv_lds_bytes<LEECH_PLANES14, 4>(a)
+                                 : gemv_lds_bytes<LEECH_PLANES14, 2>(a);
+    if (need + kTableBytes <= 160 * 1024) return w;
+  }
   return 1;
 }
 
