@@ -273,8 +273,12 @@ def test_rotate_validates_before_launch():
 
 
 def test_lane_cols_fill_the_gpu():
+    """The fewest lane_cols giving ≥ 256 tiles (4096 rows: 4, 256 tiles), halved
+    when those tiles are not whole rounds over 256 CUs (5120 rows: 320 tiles
+    at 4, so 2 and 160 tiles)."""
     from paper_2609_02652_amd._lib import LayoutDesc  # noqa: F401
-    cases = {768: 16, 1024: 16, 4096: 4, 8192: 2, 14336: 2, 16384: 1, 17408: 1}
+    cases = {768: 16, 1024: 16, 2048: 8, 3000: 4, 4096: 4, 5120: 2, 6144: 2, 7168: 2, 8192: 2,
+             14336: 1, 16384: 1, 17408: 1, 34816: 1}
     for M, C in cases.items():
         cb_ = P.Codebook(12)
         inp = synth.make_gemv_inputs(M, 24, seed=0, name="lc")
