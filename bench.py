@@ -33,7 +33,7 @@ REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Ca
 # rotated arms that mix the two forms: the activation is rotated inside the
 # GEMV's prologue up to this K (each workgroup redoes the whole transform, which
 # pays while K is small), by the separate rotation kernel above it
-ROT_IN_KERNEL_MAX_K = 4096
+ROT_IN_KERNEL_MAX_K = 5120
 ARMS = ["planes14", "slot32", "planes12x", "planes12x_inline", "golay70", "golay70_inline",
         "fp16", "noweights"]
 CONFIGS = {"c1_768x1536": (768, 1536), "c2_4096x4096": (4096, 4096),
@@ -352,7 +352,7 @@ def bench_layer(args, torch, P, synth):
             "us_fused_4_launches": res["fused"],
             "us_fused_with_rotation_8_launches": res["fused_rot"],
             "us_fused_with_rotation_in_kernel_4_launches": res["fused_rotk"],
-            "us_fused_with_rotation_in_kernel_where_K_le_4096": res["fused_rotmix"],
+            "us_fused_with_rotation_in_kernel_where_K_le_5120": res["fused_rotmix"],
             "us_fp16_7_launches": res["fp16"],
             "fusion_saves": round(1 - res["fused"] / res["separate"], 4),
             "fused_vs_fp16": round(res["fp16"] / res["fused"], 3),
@@ -484,6 +484,16 @@ def bench_step14b(args, torch, P, synth):
                 m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
         run_head()
 
+    def step_fused_rotmix(_):
+        for layer in fus:
+            for f, (m, rows) in layer.items():
+                if raw[f].numel() <= ROT_IN_KERNEL_MAX_K:
+                    m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
+                else:
+                    P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
+                    m.gemv_grouped(xrot[f], rows, [cen] * len(rows), yf[f])
+        run_head()
+
     def step_fp(_):
         for layer in fp:
             for n, w in layer.items():
@@ -494,7 +504,8 @@ def bench_step14b(args, torch, P, synth):
 
     res = {}
     for name, fn in (("separate", step_sep), ("fused", step_fused), ("fused_rot", step_fused_rot),
-                     ("fused_rotk", step_fused_rotk), ("fp16", step_fp)):
+                     ("fused_rotk", step_fused_rotk), ("fused_rotmix", step_fused_rotmix),
+                     ("fp16", step_fp)):
         res[name] = round(replay_us(torch, fn, 3), 1)
         log(f"[bench] 14B step {name}: {res[name]} us")
     head_us = round(replay_us(torch, lambda _: run_head(), 20), 1)
@@ -506,10 +517,13 @@ def bench_step14b(args, torch, P, synth):
             "head_bytes": head.numel() * 2,
             "us_separate_280": res["separate"], "us_fused_160": res["fused"],
             "us_fused_with_rotation_320": res["fused_rot"],
-            "us_fused_with_rotation_in_kernel_160": res["fused_rotk"], "us_fp16_280": res["fp16"],
+            "us_fused_with_rotation_in_kernel_160": res["fused_rotk"],
+            "us_fused_with_rotation_in_kernel_where_K_le_5120": res["fused_rotmix"],
+            "us_fp16_280": res["fp16"],
             "us_head": head_us,
             "fp16_vs_fused": round(res["fp16"] / res["fused"], 3),
             "fp16_vs_fused_with_rotation": round(res["fp16"] / res["fused_rot"], 3),
+            "fp16_vs_fused_with_rotation_mixed": round(res["fp16"] / res["fused_rotmix"], 3),
             "fp16_vs_fused_with_rotation_in_kernel": round(res["fp16"] / res["fused_rotk"], 3),
             "leech_part_GBps_fused": round(L * leech_bytes / (leech_fused * 1e-6) / 1e9, 1),
             "transcode": transcode}
