@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--no-step14b", action="store_true",
                     help="skip the 14B-class decode step (40 layers + fp16 head, Leech vs FP16)")
     ap.add_argument("--step14b-layers", type=int, default=40)
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the large single GEMVs (16384x16384, 32768x16384, 152064x5120)")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -705,6 +707,64 @@ def bench_rotation_sites(args, torch, P, synth):
     return res
 
 
+# Large single GEMVs, where the fixed cost of a launch (its dispatch gap, the
+# first loads' latency, the reduction) is small against the stream.
+LARGE = [(16384, 16384), (32768, 16384), (152064, 5120)]
+
+
+def bench_large(args, torch, P, synth):
+    """µs and served GB/s of the Planes14 GEMV on large matrices, next to the
+    FP16 control on the same decoded weights: each a graph replay over ≥ 1 GiB
+    of replicas, after the Planes14 output is checked against the FP16
+    control's (max_r |Δy_r| / (‖W_r‖·‖x‖) ≤ 2e-3)."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    dcb = P.DeviceCodebook(P.Codebook(12), dev)
+    res = {}
+    for M, K in LARGE:
+        t0 = time.time()
+        inp = synth.make_gemv_inputs(M, K, seed=5, name=f"large-{M}x{K}")
+        cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+        m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+        del cls, sm, lv
+        sb = m0.desc.served_bytes
+        reps = max(1, math.ceil(REPLICA_BYTES / sb))
+        mats = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0.clone(), m0.side1.clone(),
+                                     m0.scale.clone(), dcb) for _ in range(reps - 1)]
+        x = torch.from_numpy(inp.x).to(dev)
+        y = torch.empty(M, dtype=torch.float32, device=dev)
+        y16 = torch.empty(M, dtype=torch.float32, device=dev)
+        z, _, _ = m0.decode()
+        zf = z.float()
+        del z
+        fac = torch.from_numpy(inp.scale.astype("float32")).to(dev) / zf.pow(2).sum(-1).sqrt()
+        W = (zf * fac[..., None]).reshape(M, inp.Kpad).half().contiguous()
+        del zf, fac
+        m0.gemv(x, y)
+        P.fp16_gemv(W, x, y16)
+        torch.cuda.synchronize()
+        w_norm = np.sqrt((inp.scale.astype(np.float64) ** 2).sum(axis=1))
+        x_norm = float(np.linalg.norm(inp.x.astype(np.float64)))
+        diff = float(((y - y16).abs().double().cpu().numpy() / (w_norm * x_norm)).max())
+        if not diff <= 2e-3:
+            sys.exit(f"verification failed: large {M}x{K} planes14 vs fp16 {diff:.3g}")
+        fr = max(1, math.ceil(REPLICA_BYTES / (W.numel() * 2)))
+        Ws = [W] + [W.clone() for _ in range(fr - 1)]
+        n = 100
+        us = replay_us(torch, lambda i: mats[i % reps].gemv(x, y), n)
+        usf = replay_us(torch, lambda i: P.fp16_gemv(Ws[i % fr], x, y16), n)
+        row = {"Kpad": inp.Kpad, "lane_cols": m0.desc.lane_cols, "served_bytes": sb,
+               "us": round(us, 2), "GBps": round(sb / us / 1e3, 1),
+               "pct_hbm_peak": round(100 * sb / us / 1e3 / HBM_PEAK_GBS, 1),
+               "fp16_us": round(usf, 2), "fp16_GBps": round(W.numel() * 2 / usf / 1e3, 1),
+               "fp16_vs_planes14": round(usf / us, 3), "max_normalised_diff_vs_fp16": diff}
+        res[f"{M}x{K}"] = row
+        log(f"[bench] large {M}x{K}: {row} ({time.time() - t0:.0f}s)")
+        del mats, m0, Ws, W, inp
+        torch.cuda.empty_cache()
+    return res
+
+
 def measured_traffic(config):
     """HBM bytes per launch of the Planes14 GEMV from the committed counter
     runs (FETCH_SIZE + WRITE_SIZE, each scaled by a known-size copy), or None
@@ -828,6 +888,13 @@ def main():
         torch.cuda.synchronize()
         step14b = bench_step14b(args, torch, P, synth)
 
+    large = None
+    if not args.no_large:
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        large = bench_large(args, torch, P, synth)
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f}s")
@@ -861,6 +928,7 @@ def main():
         "batch": batch,
         "layer_8b": layer,
         "step_14b": step14b,
+        "large": large,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
