@@ -30,13 +30,17 @@
 //
 // Decode.  The paper's per-coordinate predicated tree is replaced, since the
 // MI355X has about an order of magnitude less VALU issue per HBM byte than the
-// paper's GPU: the four 24-bit planes of a block (p0, p1, p2 and the inverted
-// sign mask) are transposed 4×4 inside every nibble with eight v_bfi_b32,
-// giving one nibble per coordinate; a v_perm_b32 byte lookup in the class's
-// 8-byte table then yields two binary16 values at once, each the coordinate's
-// magnitude |z| as a subnormal (|z|·2^-24, exact) with the sign in bit 15.
-// v_dot2_f32_f16 multiplies them with x exactly and sums in f32; the block's
-// factor 2^24 · scale · centroid[gain] / (4√m) is applied once per block.
+// paper's GPU.  Every coordinate's level code (level + 1) and sign become one
+// byte-permute selector per pair of coordinates; a v_perm_b32 byte lookup in
+// the class's 8-byte table then yields two binary16 values at once, each the
+// coordinate's magnitude |z| as a subnormal (|z|·2^-24, exact) with the sign
+// in bit 15.  Planes14 records hold the codes and signs already in pair order,
+// so a selector is one rotate and one mask of a record word; the layouts that
+// hold plain planes (p0, p1, p2 and the inverted sign mask) first transpose
+// them 4×4 inside every nibble with eight v_bfi_b32 and gather the pairs.
+// v_dot2_f32_f16 multiplies the pairs with x exactly and sums in f32; the
+// block's factor 2^24 · scale · centroid[gain] / (4√m) is applied once per
+// block.
 
 #include <hip/hip_runtime.h>
 
@@ -235,15 +239,13 @@ __device__ __forceinline__ void pair_sources(uint32_t N, uint32_t s[3]) {
   s[2] = perm(R, N, 0x05050101u);
 }
 
-// Planes core: nibble (c0, c1, c2, pos) per coordinate, with c = level + 1 the
-// level code and pos = 1 for a non-negative coordinate -> 12 binary16 pairs.
-// Selector byte for the low half: the code (table bytes 1..5 hold |z| of
-// levels 0..4); for the high half: 0 (table byte 0 = 0x80) when negative, 8
-// when not (v_perm's selector 8 replicates bit 7 of table byte 1, a magnitude
-// below 0x80, giving 0x00).  Pair 3r + k of h[] covers the coordinates listed
-// by pair_sources.
-// Nibble core: the four nibble words of a block (as a Planes14 record stores
-// them) -> 12 binary16 pairs.
+// Nibble core: the four nibble words of a block (nibble g of n[r] holds the
+// level code c = level + 1 of coordinate 4g + r in bits 0..2 and its
+// non-negative bit in bit 3) -> 12 binary16 pairs; pair 3r + k of h[] covers
+// the coordinates listed by pair_sources.  Selector byte for the low half: the
+// code (table bytes 1..5 hold |z| of levels 0..4); for the high half: 0 (table
+// byte 0 = 0x80) when negative, 8 when not (v_perm's selector 8 replicates bit
+// 7 of table byte 1, a magnitude below 0x80, giving 0x00).
 __device__ __forceinline__ void nibble_core(const uint32_t n[4], uint32_t tlo, uint32_t thi,
                                             uint32_t h[12]) {
 #pragma unroll
@@ -254,6 +256,9 @@ __device__ __forceinline__ void nibble_core(const uint32_t n[4], uint32_t tlo, u
     for (int k = 0; k < 3; ++k) h[3 * r + k] = perm(thi, tlo, s[k] & 0x08070807u);
   }
 }
+// Planes core (Slot32 and Planes12x records): the bit planes of a block (p0,
+// p1, p2 the bits of each coordinate's level code, pos its non-negative bit),
+// transposed to nibbles -> 12 binary16 pairs.
 __device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p2, uint32_t pos,
                                             uint32_t tlo, uint32_t thi, uint32_t h[12]) {
   uint32_t n[4];
@@ -285,6 +290,17 @@ __host__ __device__ constexpr void pair_coords(int k, int& c0, int& c1) {
   c0 = m == 0 ? r : (m == 1 ? 4 + r : 8 + r);
   c1 = m == 0 ? 16 + r : (m == 1 ? 20 + r : 12 + r);
 }
+// The Planes14 record stores its pairs in the host's kPairCoords order, which
+// must be this one.
+__host__ __device__ constexpr bool pair_order_matches_records() {
+  for (int k = 0; k < 12; ++k) {
+    int c0 = 0, c1 = 0;
+    pair_coords(k, c0, c1);
+    if (c0 != kPairCoords[k][0] || c1 != kPairCoords[k][1]) return false;
+  }
+  return true;
+}
+static_assert(pair_order_matches_records(), "pair order of the kernels and the records");
 
 // ---------------------------------------------------------- per-block reads
 // A lane's place in a unit: its position ul (0 for a lane without a block,
