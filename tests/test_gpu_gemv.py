@@ -196,3 +196,60 @@ def test_graph_replays_match_eager(dev, dcb):
             assert torch.equal(ys[n], eager[n]), (rep, n)
         mats["planes14"].gemv(x, centroids=CEN)          # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_graph_replays_of_every_entry_point(dev, dcb):
+    """Every device entry point the bench captures (grouped, batched and
+    rotated GEMVs, the rotation, both exception decoders, the FP16 and
+    no-weights controls) gives its eager result on every replay of one HIP
+    graph, with eager work and synchronisations between the replays."""
+    M, K = 320, 1536
+    inp, (cls, sm, lv) = case(M, K, 7)
+    p14 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    g70 = P.LeechMatrix.from_fields(dcb, P.GOLAY70, cls, inp.gain, sm, lv, inp.scale, dev)
+    x = torch.from_numpy(inp.x).to(dev)
+    raw = x[:K].contiguous()
+    signs = torch.from_numpy(synth.make_signs(K, seed=7, name="graph")).to(dev)
+    X = torch.from_numpy(np.stack([synth.make_activation(K, seed=70 + b, name="graph")
+                                   for b in range(5)])).to(dev)
+    W = torch.randn(M, p14.Kpad, device=dev, dtype=torch.float16)
+    rows, cens = [256, 64], [(0.75, 1.25), (1.1, 0.9)]
+
+    out = {"grouped": torch.empty(M, device=dev), "batch": torch.empty(5, M, device=dev),
+           "rotated": torch.empty(M, device=dev), "xr": torch.empty(p14.Kpad, dtype=torch.float16,
+                                                                    device=dev),
+           "g70_inline": torch.empty(M, device=dev), "fp16": torch.empty(M, device=dev),
+           "noweights": torch.empty(M, device=dev)}
+
+    def inline(m, y):
+        P.set_exception_mode(P.EXC_INLINE)
+        try:
+            m.gemv(x, y, centroids=CEN)
+        finally:
+            P.set_exception_mode(P.EXC_HOISTED)
+
+    def enqueue():
+        p14.gemv_grouped(x, rows, cens, out["grouped"])
+        p14.gemv_batch(X, out["batch"], centroids=CEN)
+        p14.gemv_rotated(raw, signs, rows, cens, out["rotated"])
+        P.rotate_x(raw, signs, p14.Kpad, out=out["xr"])
+        inline(g70, out["g70_inline"])
+        P.fp16_gemv(W, x, out["fp16"])
+        P.noweights_ctrl(p14.desc, x, out["noweights"])
+
+    enqueue()
+    torch.cuda.synchronize()
+    eager = {k: v.clone() for k, v in out.items()}
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        enqueue()
+    for rep in range(4):
+        for v in out.values():
+            v.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in out:
+            assert torch.equal(out[k], eager[k]), (rep, k)
+        enqueue()                                # eager work between replays
+        torch.cuda.synchronize()
