@@ -253,3 +253,33 @@ def test_graph_replays_of_every_entry_point(dev, dcb):
             assert torch.equal(out[k], eager[k]), (rep, k)
         enqueue()                                # eager work between replays
         torch.cuda.synchronize()
+
+
+def test_longest_activation_and_one_block_more(dev, dcb):
+    """The activation is staged in LDS, which bounds its length.  At 8 rows
+    (lane_cols 16, so the staged blocks round up to a multiple of 16) 3024
+    blocks (Kpad 72,576) fit beside the class table and the reduction: that
+    GEMV matches the oracle and decodes bit-exactly.  3025 blocks would need a
+    190th column group and do not fit: the call is refused with LEECH_E_SHAPE
+    before any launch."""
+    M = 8
+    for nb, fits in ((3024, True), (3025, False)):
+        say(f"[longest x] {M}x{24 * nb} fits={fits}")
+        inp = synth.make_gemv_inputs(M, 24 * nb, seed=11, name="longest")
+        cb = P.Codebook(12)
+        cls, sm, lv = cb.fields_from_points(inp.z)
+        mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+        assert mat.desc.lane_cols == 16
+        x = torch.from_numpy(inp.x).to(dev)
+        if not fits:
+            with pytest.raises(P.LeechError) as e:
+                mat.gemv(x, centroids=CEN)
+            assert e.value.code == -3 and "LDS" in str(e.value)
+            continue
+        y = mat.gemv(x, centroids=CEN).cpu().numpy()
+        W = D.weights64_from_points(inp.z, inp.gain, inp.scale, CEN)
+        e = D.errors(y, D.gemv64(W, inp.x), W, inp.x)
+        assert e["max_norm_err"] <= TOL_NORM, e
+        z, c, g = mat.decode()
+        assert np.array_equal(z.cpu().numpy(), inp.z.reshape(M, nb, 24))
+        assert np.array_equal(g.cpu().numpy(), inp.gain)
