@@ -12,9 +12,9 @@
 // block, or 2048/n whole blocks); each thread owns G groups of 8 consecutive
 // coordinates.  The thread reads a group with one 16-byte load (and its signs
 // with one 8-byte load) and applies the stages of index bits 0..2 in
-// registers.  The stages of bits 3.. run in radix-8 passes through LDS: a
-// thread gathers the 8 coordinates that differ only in three bits, applies
-// their stages and scatters them back.  A last pass reads every group back in
+// registers.  The stages of bits 3.. run in passes through LDS of up to four
+// bits each: a thread gathers the coordinates that differ only in the pass's
+// bits, applies their stages and scatters them back.  A last pass reads every group back in
 // order, scales it by n^(-1/2), rounds to binary16 and writes it with 16-byte
 // stores.  The segment sits in LDS as f32 with 8 padding words per 64, which
 // keeps the stride-8 gathers of the first LDS pass on 64 distinct banks; the
@@ -74,10 +74,12 @@ __device__ __forceinline__ float h2f(uint32_t h) {
 template <int LO, int BITS, int T, int S>
 __device__ __forceinline__ void lds_pass(float* buf, int tid) {
   constexpr int E = 1 << BITS;
-  constexpr int P = S / E / T;     // groups per thread
+  constexpr int NG = S / E;                 // groups in the segment
+  constexpr int P = (NG + T - 1) / T;       // groups per thread (the last may idle)
 #pragma unroll
   for (int p = 0; p < P; ++p) {
     const int q = tid + p * T;
+    if (NG % T != 0 && q >= NG) break;
     const int b0 = ((q >> LO) << (LO + BITS)) | (q & ((1 << LO) - 1));
     float v[E];
 #pragma unroll
@@ -88,10 +90,15 @@ __device__ __forceinline__ void lds_pass(float* buf, int tid) {
   }
 }
 
+// Passes over index bits [LO, K2): the fewest of at most 4 bits each, the
+// bits spread evenly over them (k = 10: 4 + 3 rather than 3 + 3 + 1), each
+// after a barrier.  Bits are taken in increasing order, as the stages are.
 template <int LO, int K2, int T, int S>
 __device__ __forceinline__ void lds_passes(float* buf, int tid) {
   if constexpr (LO < K2) {
-    constexpr int BITS = K2 - LO < 3 ? K2 - LO : 3;
+    constexpr int left = K2 - LO;
+    constexpr int passes = (left + 3) / 4;
+    constexpr int BITS = (left + passes - 1) / passes;
     __syncthreads();
     lds_pass<LO, BITS, T, S>(buf, tid);
     lds_passes<LO + BITS, K2, T, S>(buf, tid);
