@@ -252,8 +252,10 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
 /* Batched GEMV (§6 "Batching": one decode of each weight serves several
  * activations): Y[b] = W X[b] for b < batch, X[b] binary16 [Kpad] at
  * d_X + b·ldx, Y[b] f32 [M] at d_Y + b·ldy.  Each block is decoded once per
- * launch and multiplied with up to 8 activations staged in LDS; larger
- * batches run in chunks of 8 (fewer where Kpad leaves too little LDS).  Every
+ * launch and multiplied with up to 16 activations staged in LDS; larger
+ * batches run in chunks of 16 (fewer where Kpad leaves too little LDS: 16
+ * activations fit up to about Kpad = 4,600, 8 up to about 9,200, the exact
+ * bound depending on the column groups' rounding).  Every
  * Y[b] is bit-identical to leech_gemv on X[b].  batch > 1 serves
  * LEECH_PLANES14 (LEECH_E_LAYOUT otherwise) and needs ldx ≥ Kpad, ldx a
  * multiple of 8 and ldy ≥ M (LEECH_E_ARG); batch = 1 is leech_gemv.  Other

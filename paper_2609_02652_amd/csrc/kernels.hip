@@ -761,9 +761,9 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
   return nb_vectors > 1 && xblocks * 48 >= waves * 64 * 4;
 }
 
-// NB: batch width.  Each decoded block is multiplied with NB activations
-// (NB > 1: Planes14), in the same order as a single GEMV, so every output
-// vector is bit-identical to that activation's own GEMV.
+// NB: batch width (1, 2, 4, 8 or 16).  Each decoded block is multiplied with
+// NB activations (NB > 1: Planes14), in the same order as a single GEMV, so
+// every output vector is bit-identical to that activation's own GEMV.
 // XPER: activation blocks each thread stages through registers in the ordered
 // prologue (1 when the workgroup's threads cover every block, else 2; more
 // blocks go through the unordered loop first).
@@ -1394,14 +1394,15 @@ static int launch_gemv_rotated(const GemvArgs& a, hipStream_t st) {
   return launch_gemv_kernel<LEECH_PLANES14, false, 1, 1, true>(a, shmem, st);
 }
 
-// Batch width of the next chunk of a batched launch: 2, 4 or 8 (the next
-// power of two at or above the vectors left, at most 8; vectors past the
+// Batch width of the next chunk of a batched launch: 2, 4, 8 or 16 (the next
+// power of two at or above the vectors left, at most 16; vectors past the
 // chunk's count read zero), narrowed until the activations fit in LDS; 1 for
 // a single vector left, or when not even two fit.
 static int batch_width(const GemvArgs& a, int left) {
   if (left <= 1) return 1;
-  for (int w = left > 4 ? 8 : left > 2 ? 4 : 2; w >= 2; w >>= 1) {
-    const size_t need = w == 8   ? gemv_lds_bytes<LEECH_PLANES14, 8>(a)
+  for (int w = left > 8 ? 16 : left > 4 ? 8 : left > 2 ? 4 : 2; w >= 2; w >>= 1) {
+    const size_t need = w == 16  ? gemv_lds_bytes<LEECH_PLANES14, 16>(a)
+                        : w == 8 ? gemv_lds_bytes<LEECH_PLANES14, 8>(a)
                         : w == 4 ? gemv_lds_bytes<LEECH_PLANES14, 4>(a)
                                  : gemv_lds_bytes<LEECH_PLANES14, 2>(a);
     if (need + kTableBytes <= 160 * 1024) return w;
@@ -1505,7 +1506,8 @@ int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const vo
     c.x = d_X + (int64_t)b0 * ldx;
     c.y = d_Y + (int64_t)b0 * ldy;
     c.nbatch = std::min(w, batch - b0);
-    rc = w == 8   ? launch_gemv<LEECH_PLANES14, 8>(c, st)
+    rc = w == 16  ? launch_gemv<LEECH_PLANES14, 16>(c, st)
+         : w == 8 ? launch_gemv<LEECH_PLANES14, 8>(c, st)
          : w == 4 ? launch_gemv<LEECH_PLANES14, 4>(c, st)
          : w == 2 ? launch_gemv<LEECH_PLANES14, 2>(c, st)
                   : gemv_dispatch(desc, c, st);
