@@ -364,7 +364,8 @@ int leech_rotate_x(int64_t K, int64_t Kpad, const uint16_t* d_x, const int8_t* d
  * d_bad: one u32 on the device, set to the number of codes that are not
  * format-v1 codes (their records are written as zeros; the caller must treat
  * the stream as invalid when it is nonzero).  Asynchronous on `stream`.
- * LEECH_E_LAYOUT if desc is not Planes14. */
+ * Alignment: d_main and d_index_table 16 bytes, d_code 8 (LEECH_E_ARG
+ * otherwise).  LEECH_E_LAYOUT if desc is not Planes14. */
 int leech_transcode_planes14(const leech_layout_desc* desc, const void* d_index_table,
                              const uint64_t* d_code, void* d_main, uint32_t* d_bad,
                              void* stream);

@@ -81,6 +81,18 @@ __host__ __device__ inline uint32_t idx_extract(uint32_t v, uint32_t mask) {
   return out;
 }
 
+// q = a / d and a − q·d for a < 2^48 and 0 < d < 2^48: both convert to double
+// exactly, the rounded quotient is within one of the true one, and one integer
+// correction in each direction makes it exact.  (A 64-bit integer division is
+// a long instruction sequence on the GPU; this is a handful.)
+__host__ __device__ inline uint64_t idx_divmod(uint64_t a, uint64_t d, uint64_t* rem) {
+  uint64_t q = (uint64_t)((double)a / (double)d);
+  if (q * d > a) --q;
+  else if (a - q * d >= d) ++q;
+  *rem = a - q * d;
+  return q;
+}
+
 __host__ __device__ inline int idx_find_class(const IdxTable& T, uint64_t idx) {
   int lo = 0, hi = (int)T.n_classes - 1;     // largest c with offset(c) ≤ idx
   while (lo < hi) {
@@ -115,8 +127,9 @@ __host__ __device__ inline void idx_place(const IdxTable& T, const IdxClass& c, 
   for (int k = kMaxLevels - 1; k >= 0; --k) {
     digit[k] = 0;
     if (radix[k] > 1) {
-      digit[k] = (uint32_t)(a % radix[k]);
-      a /= radix[k];
+      uint64_t rem;
+      a = idx_divmod(a, radix[k], &rem);
+      digit[k] = (uint32_t)rem;
     }
   }
   const int last = idx_top(on);
@@ -197,10 +210,10 @@ __host__ __device__ inline bool idx_decode(const IdxTable& T, uint64_t code, uin
     r >>= c.f2;
     const uint32_t s_off = (uint32_t)(r & ((1ull << c.f0) - 1));
     r >>= c.f0;
-    const uint64_t a_off = r % c.B;
-    r /= c.B;
-    const uint64_t a_sup = r % c.A;
-    const uint32_t cw = T.cw_weight[T.weight_start[c.w] + (uint32_t)(r / c.A)];
+    uint64_t a_off, a_sup;
+    r = idx_divmod(r, c.B, &a_off);
+    const uint64_t k_cw = idx_divmod(r, c.A, &a_sup);
+    const uint32_t cw = T.cw_weight[T.weight_start[c.w] + (uint32_t)k_cw];
     idx_place(T, c, c.side, cw, a_sup, planes, &zero, &mag3);
     idx_place(T, c, all_levels & ~(uint32_t)c.side, ~cw & 0xFFFFFFu, a_off, planes, &zero, &mag3);
     // flipping an off-support coordinate (|z| ≡ 0 mod 4) moves Σz by a multiple
@@ -210,8 +223,9 @@ __host__ __device__ inline bool idx_decode(const IdxTable& T, uint64_t code, uin
     neg = idx_deposit(s_off, ~zero & ~cw & 0xFFFFFFu) | idx_deposit(s_sup, cw & ~top);
     if (top && ((c.sum8 + 4 * idx_popc(neg & cw)) & 7)) neg |= top;
   } else {
-    const uint64_t a_all = r % c.A;
-    const uint32_t cw = T.cw_value[(uint32_t)(r / c.A)];
+    uint64_t a_all;
+    const uint64_t k_cw = idx_divmod(r, c.A, &a_all);
+    const uint32_t cw = T.cw_value[(uint32_t)k_cw];
     idx_place(T, c, all_levels, 0xFFFFFFu, a_all, planes, &zero, &mag3);
     neg = cw ^ mag3;
   }

@@ -25,7 +25,9 @@
 namespace leech {
 namespace {
 
-constexpr int kTcThreads = 256;
+constexpr int kTcThreads = 512;
+static_assert(sizeof(IdxTable) % 16 == 0, "the table is copied to LDS in 16-byte words");
+constexpr int kTcBlocksPerCu = 2;     // two workgroups (each with its LDS table copy) per CU
 constexpr int kRecsPerThread = 8;
 constexpr int kBytesPerThread = kRecsPerThread * kPlanes14Bytes;   // 112 = 7 × 16
 
@@ -44,7 +46,8 @@ struct TranscodeArgs {
 // Record words of one block: its three pair words and the 16-bit
 // class | gain << 9 (the record's last two bytes).  Zeros for slots
 // past the matrix and for codes that are not format-v1 codes.
-__device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, uint32_t w[4]) {
+__device__ __forceinline__ void record_words(const TranscodeArgs& a, const IdxTable& T, int64_t s,
+                                             uint32_t w[4]) {
   w[0] = w[1] = w[2] = w[3] = 0;
   if (s >= a.n) return;
   const int64_t t = s / a.tile_blocks;
@@ -58,7 +61,7 @@ __device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, 
   uint16_t cls;
   uint8_t gain;
   uint32_t smask, p[3];
-  if (!idx_decode(*a.T, a.code[r * a.nb + j], &cls, &gain, &smask, p)) {
+  if (!idx_decode(T, a.code[r * a.nb + j], &cls, &gain, &smask, p)) {
     atomicAdd(a.bad, 1u);
     return;
   }
@@ -71,6 +74,16 @@ __device__ __forceinline__ void record_words(const TranscodeArgs& a, int64_t s, 
 }
 
 __global__ __launch_bounds__(kTcThreads) void transcode_planes14_kernel(TranscodeArgs a) {
+  // the index table (60.7 KB) in LDS: the class search, the binomials of the
+  // colex unranking and the codeword lists are then LDS reads, not a chain of
+  // dependent L2 reads per block
+  __shared__ __attribute__((aligned(16))) IdxTable tab;
+  {
+    const u32x4t* src = reinterpret_cast<const u32x4t*>(a.T);
+    u32x4t* dst = reinterpret_cast<u32x4t*>(&tab);
+    for (int i = threadIdx.x; i < (int)(sizeof(IdxTable) / 16); i += kTcThreads) dst[i] = src[i];
+  }
+  __syncthreads();
   const int64_t stride = (int64_t)gridDim.x * kTcThreads;
   for (int64_t t = (int64_t)blockIdx.x * kTcThreads + threadIdx.x;
        (uint64_t)t * kBytesPerThread < a.main_bytes; t += stride) {
@@ -78,8 +91,8 @@ __global__ __launch_bounds__(kTcThreads) void transcode_planes14_kernel(Transcod
 #pragma unroll
     for (int i = 0; i < kRecsPerThread; i += 2) {
       uint32_t x[4], y[4];
-      record_words(a, t * kRecsPerThread + i, x);
-      record_words(a, t * kRecsPerThread + i + 1, y);
+      record_words(a, tab, t * kRecsPerThread + i, x);
+      record_words(a, tab, t * kRecsPerThread + i + 1, y);
       // two 14-byte records = seven words: the second starts at byte 14
       const int b = i / 2 * 7;
       out[b + 0] = x[0];
@@ -130,7 +143,7 @@ extern "C" int leech_transcode_planes14(const leech_layout_desc* desc, const voi
   const int64_t n = desc->M * desc->nb;
   if (desc->main_bytes != (uint64_t)n * kPlanes14Bytes + kPadBytes)
     return set_error(LEECH_E_SHAPE, "descriptor size is not the Planes14 size of its shape");
-  if (((uintptr_t)d_main & 15) || ((uintptr_t)d_code & 7) || ((uintptr_t)d_index_table & 7))
+  if (((uintptr_t)d_main & 15) || ((uintptr_t)d_code & 7) || ((uintptr_t)d_index_table & 15))
     return set_error(LEECH_E_ARG, "misaligned device pointer");
   Geometry geo(desc->M, desc->nb, desc->lane_cols);
   TranscodeArgs a;
@@ -147,7 +160,11 @@ extern "C" int leech_transcode_planes14(const leech_layout_desc* desc, const voi
   a.C = geo.C;
   a.R = geo.R;
   const uint64_t threads = (desc->main_bytes + kBytesPerThread - 1) / kBytesPerThread;
-  const uint64_t blocks = std::min<uint64_t>((threads + kTcThreads - 1) / kTcThreads, 8192);
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess)
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const uint64_t blocks = std::min<uint64_t>((threads + kTcThreads - 1) / kTcThreads,
+                                             (uint64_t)kTcBlocksPerCu * (uint64_t)std::max(cus, 1));
   hipLaunchKernelGGL(clear_u32_kernel, dim3(1), dim3(1), 0, (hipStream_t)stream, d_bad);
   hipLaunchKernelGGL(transcode_planes14_kernel, dim3((unsigned)blocks), dim3(kTcThreads), 0,
                      (hipStream_t)stream, a);
