@@ -31,9 +31,16 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published peak
 REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Cache
 # rotated arms that mix the two forms: the activation is rotated inside the
-# GEMV's prologue up to this K (each workgroup redoes the whole transform, which
-# pays while K is small), by the separate rotation kernel above it
+# GEMV's prologue up to this K and this many workgroups (each workgroup redoes
+# the whole transform, which pays while K is small and the workgroups few), by
+# the separate rotation kernel otherwise
 ROT_IN_KERNEL_MAX_K = 5120
+ROT_IN_KERNEL_MAX_TILES = 512
+
+
+def rotate_in_kernel(m, K):
+    tiles = -(-m.desc.M // (64 // m.desc.lane_cols))
+    return K <= ROT_IN_KERNEL_MAX_K and tiles <= ROT_IN_KERNEL_MAX_TILES
 ARMS = ["planes14", "slot32", "planes12x", "planes12x_inline", "golay70", "golay70_inline",
         "fp16", "noweights"]
 CONFIGS = {"c1_768x1536": (768, 1536), "c2_4096x4096": (4096, 4096),
@@ -308,10 +315,10 @@ def bench_layer(args, torch, P, synth):
         for f, (m, rows) in fus_r[i % reps].items():
             m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
 
-    # in the prologue where K ≤ ROT_IN_KERNEL_MAX_K, a separate rotation above
+    # in the prologue where rotate_in_kernel says so, a separate rotation otherwise
     def run_fused_rotmix(i):
         for f, (m, rows) in fus_r[i % reps].items():
-            if raw[f].numel() <= ROT_IN_KERNEL_MAX_K:
+            if rotate_in_kernel(m, raw[f].numel()):
                 m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
             else:
                 P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
@@ -354,7 +361,7 @@ def bench_layer(args, torch, P, synth):
             "us_fused_4_launches": res["fused"],
             "us_fused_with_rotation_8_launches": res["fused_rot"],
             "us_fused_with_rotation_in_kernel_4_launches": res["fused_rotk"],
-            "us_fused_with_rotation_in_kernel_where_K_le_5120": res["fused_rotmix"],
+            "us_fused_with_rotation_mixed": res["fused_rotmix"],
             "us_fp16_7_launches": res["fp16"],
             "fusion_saves": round(1 - res["fused"] / res["separate"], 4),
             "fused_vs_fp16": round(res["fp16"] / res["fused"], 3),
@@ -489,7 +496,7 @@ def bench_step14b(args, torch, P, synth):
     def step_fused_rotmix(_):
         for layer in fus:
             for f, (m, rows) in layer.items():
-                if raw[f].numel() <= ROT_IN_KERNEL_MAX_K:
+                if rotate_in_kernel(m, raw[f].numel()):
                     m.gemv_rotated(raw[f], signs[f], rows, [cen] * len(rows), yf[f])
                 else:
                     P.rotate_x(raw[f], signs[f], m.Kpad, out=xrot[f])
@@ -520,7 +527,7 @@ def bench_step14b(args, torch, P, synth):
             "us_separate_280": res["separate"], "us_fused_160": res["fused"],
             "us_fused_with_rotation_320": res["fused_rot"],
             "us_fused_with_rotation_in_kernel_160": res["fused_rotk"],
-            "us_fused_with_rotation_in_kernel_where_K_le_5120": res["fused_rotmix"],
+            "us_fused_with_rotation_mixed": res["fused_rotmix"],
             "us_fp16_280": res["fp16"],
             "us_head": head_us,
             "fp16_vs_fused": round(res["fp16"] / res["fused"], 3),

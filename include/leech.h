@@ -152,10 +152,10 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  * Records are stored in "wave tile" order: rows are grouped in tiles of
  * tile_rows = 64 / lane_cols rows; within a tile, each run of lane_cols
  * consecutive blocks of the tile's rows forms one 64-block unit, stored row by
- * row.  lane_cols (1, 2, 4, 8 or 16) is chosen from M: the fewest that give
- * at least 256 tiles (one per CU), halved when that many tiles would not be a
- * whole number of rounds over the 256 CUs; the kernels read one unit per
- * wavefront step.
+ * row.  lane_cols (1, 2, 4, 8 or 16) is chosen from M to even out the CUs'
+ * work: the least ceil(tiles / 256) · (tile_rows + 8), ties to fewer tiles
+ * (4096 rows: 4; 5120: 2; 8192: 2; 17408: 2; 28672: 1); the kernels read one
+ * unit per wavefront step.
  */
 enum { LEECH_SLOT32 = 0, LEECH_PLANES14 = 1, LEECH_PLANES12X = 2, LEECH_GOLAY70 = 3 };
 

@@ -39,7 +39,7 @@ def activations(K, B, seed):
 
 
 @pytest.mark.parametrize("M,K,B", [(1, 24, 2), (65, 408, 3), (257, 792, 8), (768, 1536, 5),
-                                   (4096, 4096, 11), (16385, 120, 4), (1024, 17408, 8),
+                                   (4096, 4096, 11), (14337, 120, 4), (1024, 17408, 8),
                                    (300, 24 * 30, 1), (768, 1536, 21), (257, 792, 16)])
 def test_batch_matches_single_and_oracle(dev, dcb, M, K, B):
     say(f"[batch] {M}x{K} B={B}")

@@ -98,7 +98,8 @@ def test_model_14b_shapes(dev, dcb, proj):
 
 def test_odd_last_tile_all_layouts(dev, dcb):
     """lane_cols 1 with a one-row last tile: unit bases that are not 4-aligned."""
-    check_matrix(dev, dcb, "tall-odd", 16385, 24 * 5, seed=7,
+    assert P.planes14_desc(14337, 24 * 5).lane_cols == 1
+    check_matrix(dev, dcb, "tall-odd", 14337, 24 * 5, seed=7,
                  layouts=("planes14", "slot32", "planes12x", "golay70"), rows_sampled=256)
 
 

@@ -96,7 +96,7 @@ def test_no_index_for_balls_past_2_47():
         big.table(_lib.TABLE_INDEX)
 
 
-@pytest.mark.parametrize("M,K", [(1, 24), (65, 408), (257, 792), (16385, 120), (4096, 4104)])
+@pytest.mark.parametrize("M,K", [(1, 24), (65, 408), (257, 792), (14337, 120), (4096, 4104)])
 def test_planes14_desc_matches_expansion(cb, M, K):
     d = P.planes14_desc(M, K)
     if M * K > 2_000_000:

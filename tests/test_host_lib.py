@@ -273,12 +273,12 @@ def test_rotate_validates_before_launch():
 
 
 def test_lane_cols_fill_the_gpu():
-    """The fewest lane_cols giving ≥ 256 tiles (4096 rows: 4, 256 tiles), halved
-    when those tiles are not whole rounds over 256 CUs (5120 rows: 320 tiles
-    at 4, so 2 and 160 tiles)."""
+    """lane_cols minimises ceil(tiles / 256) · (rows per tile + 8): 4096 rows
+    take 4 (256 tiles of 16), 5120 rows 2 (160 of 32 rather than 320 of 16),
+    17408 rows 2 (544 of 32 rather than 272 of 64), 28672 rows 1."""
     from paper_2609_02652_amd._lib import LayoutDesc  # noqa: F401
-    cases = {768: 16, 1024: 16, 2048: 8, 3000: 4, 4096: 4, 5120: 2, 6144: 2, 7168: 2, 8192: 2,
-             14336: 1, 16384: 1, 17408: 1, 34816: 1}
+    cases = {1: 16, 768: 16, 1024: 16, 2048: 8, 3000: 4, 4096: 4, 5120: 2, 6144: 2, 7168: 2,
+             8192: 2, 14336: 1, 14337: 1, 16384: 1, 17408: 2, 28672: 1, 34816: 2, 152064: 1}
     for M, C in cases.items():
         cb_ = P.Codebook(12)
         inp = synth.make_gemv_inputs(M, 24, seed=0, name="lc")
