@@ -71,6 +71,8 @@ def parse():
     ap.add_argument("--no-step14b", action="store_true",
                     help="skip the 14B-class decode step (40 layers + fp16 head, Leech vs FP16)")
     ap.add_argument("--step14b-layers", type=int, default=40)
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time square Planes14 GEMVs from 1024x1024 to 16384x16384")
     ap.add_argument("--no-large", action="store_true",
                     help="skip the large single GEMVs (16384x16384, 32768x16384, 152064x5120)")
     ap.add_argument("--calib-mib", type=int, default=0,
@@ -772,6 +774,45 @@ def bench_large(args, torch, P, synth):
     return res
 
 
+SWEEP = [1024, 2048, 3072, 4096, 6144, 8192, 12288, 16384]
+
+
+def bench_sweep(args, torch, P, synth):
+    """Square Planes14 GEMVs from 1024² to 16384² next to the FP16 control
+    (random fp16 weights of the same shape: its time depends on the bytes
+    only), each a graph replay over ≥ 1 GiB of replicas: where the fixed cost
+    of a launch stops mattering."""
+    dev = torch.device("cuda:0")
+    dcb = P.DeviceCodebook(P.Codebook(12), dev)
+    res = {}
+    for n in SWEEP:
+        inp = synth.make_gemv_inputs(n, n, seed=8, name=f"sweep-{n}")
+        cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+        m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+        del cls, sm, lv
+        sb = m0.desc.served_bytes
+        reps = max(1, math.ceil(REPLICA_BYTES / sb))
+        mats = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0.clone(), m0.side1.clone(),
+                                     m0.scale.clone(), dcb) for _ in range(reps - 1)]
+        x = torch.from_numpy(inp.x).to(dev)
+        y = torch.empty(n, dtype=torch.float32, device=dev)
+        W = torch.randn(n, inp.Kpad, device=dev, dtype=torch.float16)
+        fr = max(1, math.ceil(REPLICA_BYTES / (W.numel() * 2)))
+        Ws = [W] + [W.clone() for _ in range(fr - 1)]
+        steps = 300 if sb < 5e7 else 100
+        us = replay_us(torch, lambda i: mats[i % reps].gemv(x, y), steps)
+        usf = replay_us(torch, lambda i: P.fp16_gemv(Ws[i % fr], x, y), steps)
+        row = {"Kpad": inp.Kpad, "lane_cols": m0.desc.lane_cols, "served_bytes": sb,
+               "us": round(us, 2), "GBps": round(sb / us / 1e3, 1),
+               "pct_hbm_peak": round(100 * sb / us / 1e3 / HBM_PEAK_GBS, 1),
+               "fp16_us": round(usf, 2), "fp16_GBps": round(W.numel() * 2 / usf / 1e3, 1)}
+        res[str(n)] = row
+        log(f"[bench] sweep {n}x{n}: {row}")
+        del mats, m0, Ws, W, inp
+        torch.cuda.empty_cache()
+    return res
+
+
 def measured_traffic(config):
     """HBM bytes per launch of the Planes14 GEMV from the committed counter
     runs (FETCH_SIZE + WRITE_SIZE, each scaled by a known-size copy), or None
@@ -901,6 +942,13 @@ def main():
         torch.cuda.synchronize()
         large = bench_large(args, torch, P, synth)
 
+    sweep = None
+    if args.sweep:
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        sweep = bench_sweep(args, torch, P, synth)
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f}s")
@@ -935,6 +983,7 @@ def main():
         "layer_8b": layer,
         "step_14b": step14b,
         "large": large,
+        "sweep": sweep,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
