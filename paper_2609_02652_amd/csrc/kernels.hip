@@ -571,6 +571,21 @@ __device__ __forceinline__ float dot12(const uint32_t h[12], const uint32_t xw[1
   return s;
 }
 
+// Sum over the C lanes of a row (C = 1, 2, 4, 8 or 16 adjacent lanes) as an
+// xor butterfly, partners 1, 2, 4, 8 apart in that order: within a quad by DPP
+// quad permutes, across quads by ds_swizzle's xor mode (no address register,
+// no LDS memory).  Every lane is active here.
+__device__ __forceinline__ float row_sum(float v, int C) {
+  auto add = [&](int partner) { v += __builtin_bit_cast(float, partner); };
+  if (C > 1)
+    add(__builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+  if (C > 2)
+    add(__builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+  if (C > 4) add(__builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (4 << 10) | 0x1F));
+  if (C > 8) add(__builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), (8 << 10) | 0x1F));
+  return v;
+}
+
 // ------------------------------------------------------- fused rotation
 // The activation rotation (blockwise Walsh–Hadamard, §2.3, §6) done by each
 // GEMV workgroup in its prologue, while its first record loads are in flight:
@@ -1173,8 +1188,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    float v = acc[b];
-    for (int off = 1; off < C; off <<= 1) v += __shfl_xor(v, off);
+    const float v = row_sum(acc[b], C);
     if (cl == 0 && rl < R_t) red[(b * waves + wave) * 64 + rl] = v;
   }
   __syncthreads();
