@@ -75,6 +75,9 @@ def parse():
                     help="also time square Planes14 GEMVs from 1024x1024 to 16384x16384")
     ap.add_argument("--no-large", action="store_true",
                     help="skip the large single GEMVs (16384x16384, 32768x16384, 152064x5120)")
+    ap.add_argument("--no-floor", action="store_true",
+                    help="skip the launch-floor probe (one-element fill, one-block GEMV)")
+    ap.add_argument("--floor-steps", type=int, default=2000)
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -830,6 +833,54 @@ def measured_traffic(config):
     return c["traffic_bytes"] if c else None
 
 
+def bench_floor(args, torch, P, synth):
+    """The per-launch floor under graph replay: µs per launch of a one-element
+    torch fill (the smallest kernel the runtime launches), of the no-weights
+    control and of the Planes14 GEMV on one 24-wide block (one tile, one
+    unit), and of both at the bench shape with a single cache-resident copy
+    of the records.  Each is one replay of a graph of args.floor_steps
+    launches, best of five; the bench shape's fraction of peak with the fill's
+    floor taken out is reported beside it."""
+    dev = torch.device("cuda:0")
+    n = args.floor_steps
+
+    def per_launch(fn):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(n):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(5):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) * 1e3 / n)
+        del g
+        return round(best, 3)
+
+    t = torch.zeros(1, device=dev)
+    out = {"launches_per_graph": n, "fill_one_element_us": per_launch(lambda: t.fill_(1.0))}
+    dcb = P.DeviceCodebook(P.Codebook(12), dev)
+    for tag, (M, K) in (("one_block", (64, 24)), ("bench_shape_cached", CONFIGS[args.config])):
+        inp = synth.make_gemv_inputs(M, K, seed=args.seed, name="launch-floor")
+        cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+        m = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+        x = torch.from_numpy(inp.x).to(dev)
+        y = torch.empty(M, dtype=torch.float32, device=dev)
+        out[tag] = {"M": M, "K": K,
+                    "planes14_us": per_launch(lambda: m.gemv(x, y)),
+                    "noweights_us": per_launch(lambda: P.noweights_ctrl(m.desc, x, y))}
+    log(f"[bench] launch floor: {out}")
+    return out
+
+
 def cpu_baseline(inp, seconds):
     """The oracle as it stands, on the host: decode every block from its
     fields, form the f64 weights and multiply, repeated for about `seconds`.
@@ -949,6 +1000,17 @@ def main():
         torch.cuda.synchronize()
         sweep = bench_sweep(args, torch, P, synth)
 
+    floor = None
+    if not args.no_floor:
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        floor = bench_floor(args, torch, P, synth)
+        f = floor["fill_one_element_us"]
+        if us > f:
+            floor["pct_hbm_peak_above_fill_floor"] = round(
+                100 * main_arm.served_bytes / ((us - f) * 1e-6) / 1e9 / HBM_PEAK_GBS, 1)
+
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] timing the CPU oracle for ~{args.cpu_seconds:.0f}s")
@@ -984,6 +1046,7 @@ def main():
         "step_14b": step14b,
         "large": large,
         "sweep": sweep,
+        "launch_floor": floor,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
