@@ -39,6 +39,11 @@ taken here:
   theirs, with radix C(free, c).  (The positions of the largest magnitude are
   forced: radix 1.)  The product of the radices is the multinomial
   coefficient, so every digit string names exactly one arrangement.
+
+Parity with the paper's own codes is unpinned: the paper prints none.  The
+tests pin this map by what any such index must satisfy (a bijection onto the
+ball, round trips of every class's first and last index, the class sizes)
+and fix its order with a stored fingerprint written from this module.
 """
 from __future__ import annotations
 
