@@ -14,8 +14,9 @@ repeated reads: the bytes come from HBM.
 Printed: one JSON line with the metric (served-weight GB/s of the Planes14
 GEMV), µs per GEMV, the roofline against MI355X's 8 TB/s, every arm of the
 layout comparison (four layouts, FP16 GEMV control, no-weights control;
-interleaved, 7 rounds, first 2 discarded, medians) and the CPU oracle timed on
-a bounded sample of the same workload.
+interleaved, 7 rounds, first 2 discarded, medians), the decoder-layer,
+batch, large-matrix and launch-floor sections, and the CPU oracle timed on a
+bounded sample of the same workload.
 """
 import argparse
 import json
