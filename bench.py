@@ -7,9 +7,14 @@ A step is one GEMV y = W x of the workload matrix in the served layout
 (Planes14, 4.80 b/w records + fp16 per-block scales), with W and x resident in
 HBM.  The timed region is exactly K steps, bracketed by a device
 synchronisation on both sides and timed with HIP events on the launch stream.
-Each step reads a different replica of the matrix (same codes, distinct
-buffers, ≥ 1 GB in total) so that the 256 MB Infinity Cache cannot serve
-repeated reads: the bytes come from HBM.
+The matrix is held in n replicas (same codes, distinct buffers, ≥ 1 GiB in
+all); step j reads replica j mod n.  Right before the timed replay, a replay
+of the replicas the timed region does not read (or, when K leaves fewer than
+512 MiB of them, of every replica) streams ≥ 512 MiB, twice the 256 MB
+Infinity Cache, so no replica the timed region reads can still be cached: its
+bytes come from HBM.  The line states the timed bytes, the working set and the
+fewest bytes streamed between a replica's previous read and its timed read,
+and the same GEMV timed over one whole ≥ 1 GiB cycle of replicas beside it.
 
 Printed: one JSON line with the metric (served-weight GB/s of the Planes14
 GEMV), µs per GEMV, the roofline against MI355X's 8 TB/s, every arm of the
@@ -31,6 +36,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published peak
 REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Cache
+EVICT_BYTES = 512 << 20        # streamed right before a timed replay: 2× that cache
 # rotated arms that mix the two forms: the activation is rotated inside the
 # GEMV's prologue up to this K and this many workgroups (each workgroup redoes
 # the whole transform, which pays while K is small and the workgroups few), by
@@ -79,6 +85,9 @@ def parse():
     ap.add_argument("--no-floor", action="store_true",
                     help="skip the launch-floor probe (one-element fill, one-block GEMV)")
     ap.add_argument("--floor-steps", type=int, default=2000)
+    ap.add_argument("--no-arms-c4", action="store_true",
+                    help="skip the 8192x8192 layout sweep (four layouts, both exception "
+                         "decoders, FP16 and no-weights controls)")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -98,22 +107,35 @@ class Arm:
         for s in range(start, start + k):
             self.launchers[s % n]()
 
-    def graph(self, torch, k):
-        """A HIP graph of k consecutive GEMVs (replicas in turn), captured once:
-        replaying it enqueues the k kernels without k host round trips."""
-        if k not in self._graphs:
+    def graph(self, torch, k, start=0):
+        """A HIP graph of k consecutive GEMVs over replicas start, start + 1, …
+        (mod n), captured once: replaying it enqueues the k kernels without k
+        host round trips."""
+        key = (k, start)
+        if key not in self._graphs:
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                self.run(k)
-            self._graphs[k] = g
-        return self._graphs[k]
+                self.run(k, start)
+            self._graphs[key] = g
+        return self._graphs[key]
+
+    def evict_plan(self, k):
+        """The replay that precedes a timed replay of k GEMVs from replica 0:
+        (start, length) of the replicas it reads, and the fewest bytes streamed
+        between a timed replica's previous read and its timed read.  It reads
+        only the replicas the timed region does not read when those hold
+        ≥ EVICT_BYTES, else one whole cycle from replica 0."""
+        n, b = len(self.launchers), max(self.served_bytes, 1)
+        if (n - k) * b >= EVICT_BYTES:
+            return k, n - k, (n - k) * b
+        return 0, n, (n - 1) * b
 
 
-def build_arms(args, torch, P, synth):
-    M, K = CONFIGS[args.config]
+def build_arms(args, torch, P, synth, config=None):
+    M, K = CONFIGS[config or args.config]
     dev = torch.device("cuda:0")
     t0 = time.time()
-    inp = synth.make_gemv_inputs(M, K, seed=args.seed, name=args.config)
+    inp = synth.make_gemv_inputs(M, K, seed=args.seed, name=config or args.config)
     cb = P.Codebook(12)
     dcb = P.DeviceCodebook(cb, dev)
     cls, sm, lv = cb.fields_from_points(inp.z)
@@ -215,8 +237,13 @@ def verify_arms(torch, inp, arms, y):
 
 def time_arm(torch, arm, steps):
     """ms for `steps` GEMVs: one replay of a graph holding exactly `steps`
-    launches, bracketed by device synchronisations and timed with HIP events
-    on the stream the kernels run on."""
+    launches (replicas 0, 1, …), bracketed by device synchronisations and
+    timed with HIP events on the stream the kernels run on.  The replay of
+    arm.evict_plan(steps) runs first, outside the timed region, so that the
+    timed replicas are read from HBM."""
+    start, length, _ = arm.evict_plan(steps)
+    if arm.served_bytes:
+        arm.graph(torch, length, start).replay()
     g = arm.graph(torch, steps)
     st = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
@@ -227,6 +254,130 @@ def time_arm(torch, arm, steps):
     e1.record(st)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1)
+
+
+def cycle_us(torch, arm, replays=3):
+    """µs per GEMV over one whole cycle of the arm's replicas (≥ 1 GiB), median
+    of `replays` timed replays after one untimed one."""
+    n = len(arm.launchers)
+    g = arm.graph(torch, n)
+    g.replay()
+    out = []
+    for _ in range(replays):
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1) * 1e3 / n)
+    return statistics.median(out)
+
+
+def arms_table(args, torch, arms, inp):
+    """§3.1's comparison: every arm timed as a k-GEMV replay, arms interleaved
+    in a fixed order for args.rounds rounds, the first args.discard dropped;
+    medians with min and max, and the median of the per-round ratios against
+    the FP16 control."""
+    k_arm = max(200, args.steps // 4)
+    per_round = {n: [] for n in arms}
+    for r in range(args.rounds):
+        for n, a in arms.items():
+            per_round[n].append(time_arm(torch, a, k_arm) * 1e3 / k_arm)
+        log(f"[bench] {inp.M}x{inp.K} round {r + 1}/{args.rounds} done")
+    kept = {n: v[args.discard:] for n, v in per_round.items()}
+    table = {}
+    for n, v in kept.items():
+        med = statistics.median(v)
+        row = {"us_per_gemv": round(med, 3), "min_us": round(min(v), 3), "max_us": round(max(v), 3),
+               "served_bytes": arms[n].served_bytes}
+        if arms[n].served_bytes:
+            row["GBps"] = round(arms[n].served_bytes / (med * 1e-6) / 1e9, 1)
+            row["pct_hbm_peak"] = round(100 * row["GBps"] / HBM_PEAK_GBS, 1)
+            row["bits_per_weight"] = round(8 * arms[n].served_bytes / (inp.M * inp.Kpad), 3)
+        if "fp16" in kept:
+            ratios = [f / t for f, t in zip(kept["fp16"], v)]
+            row["vs_fp16"] = round(statistics.median(ratios), 3)
+        table[n] = row
+    return table
+
+
+def prologue_table(args, torch, P, arm):
+    """µs per GEMV of the arm under each prologue mode (the order in which
+    waves request their records; leech_set_prologue_mode), as cold-replica
+    timed replays of 200 launches, modes interleaved over 5 rounds: the
+    measurement behind the automatic choice."""
+    k = 200
+    res = {m: [] for m in ("auto", 0, 1, 2)}
+    graphs = {}
+    try:
+        for m in res:
+            P.set_prologue_mode(P.PROLOGUE_AUTO if m == "auto" else m)
+            arm._graphs.clear()
+            start, length, _ = arm.evict_plan(k)
+            graphs[m] = (arm.graph(torch, length, start), arm.graph(torch, k))
+        arm._graphs.clear()
+    finally:
+        P.set_prologue_mode(P.PROLOGUE_AUTO)
+    for _ in range(5):
+        for m, (ev, g) in graphs.items():
+            ev.replay()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            res[m].append(e0.elapsed_time(e1) * 1e3 / k)
+    del graphs
+    return {str(m): round(statistics.median(v), 3) for m, v in res.items()}
+
+
+def shader_clock(torch, arm, seconds=1.0):
+    """The shader clock while the arm's GEMVs run back to back: the current
+    level of /sys/class/drm/card*/device/pp_dpm_sclk, sampled every 20 ms
+    during about `seconds` of graph replays (median and range in MHz), or None
+    where the file cannot be read."""
+    import glob
+    import re
+    import threading
+    paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+    samples, stop = [], []
+
+    def poll():
+        while not stop:
+            for p in paths:
+                try:
+                    for line in open(p).read().splitlines():
+                        m = re.match(r"\s*\d+:\s*(\d+)\s*[Mm][Hh]z\s*\*", line)
+                        if m:
+                            samples.append(int(m.group(1)))
+                except OSError:
+                    pass
+            time.sleep(0.02)
+
+    if not paths:
+        return None
+    n = len(arm.launchers)
+    g = arm.graph(torch, n)
+    g.replay()
+    torch.cuda.synchronize()
+    th = threading.Thread(target=poll)
+    th.start()
+    t0 = time.time()
+    while time.time() - t0 < seconds:
+        for _ in range(10):
+            g.replay()
+        torch.cuda.synchronize()
+    stop.append(1)
+    th.join()
+    if not samples:
+        return None
+    return {"median_MHz": statistics.median(samples), "min_MHz": min(samples),
+            "max_MHz": max(samples), "samples": len(samples),
+            "source": "pp_dpm_sclk during back-to-back GEMV replays", "max_rated_MHz": 2400}
 
 
 # One 8B-class decoder layer at batch 1: (name, rows, K), K padded to 24.
@@ -882,32 +1033,69 @@ def bench_floor(args, torch, P, synth):
     return out
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(inp, seconds):
-    """The oracle as it stands, on the host: decode every block from its
-    fields, form the f64 weights and multiply, repeated for about `seconds`.
-    numpy runs the decode and the weights on one thread; the BLAS pool behind
-    the final matvec is held to one thread as well, so the figure is one
-    core's."""
+    """The oracle as it stands, on the host (the benchmark's CPU plan): (a) decode
+    every block from its fields, form the f64 weights and multiply, and (b)
+    the f64 matvec alone on the decoded weights, each repeated for about a
+    quarter of `seconds`, once with the BLAS pool held to one thread and once
+    with it on every core this process may use.  numpy runs the decode and the
+    weights on one thread either way.  The reported value is (a) on every
+    core; the four legs are listed beside it."""
     from threadpoolctl import threadpool_limits
     from oracle import decode as D
     cls, sm, lv = D.fields_from_points(inp.z)           # setup, not timed
     served = inp.M * inp.nb * 16
-    with threadpool_limits(limits=1):
-        n, t0 = 0, time.perf_counter()
-        while True:
-            z = D.decode_fields(cls, sm, lv)
-            W = D.weights64(cls, inp.gain, inp.scale, z)
-            y = D.gemv64(W, inp.x)
-            n += 1
-            el = time.perf_counter() - t0
-            if el >= seconds or n >= 1000:
-                break
-    del y
-    return {"value": served * n / el / 1e9, "unit": "GB/s", "cores": 1,
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    W0 = D.weights64(cls, inp.gain, inp.scale, D.decode_fields(cls, sm, lv))
+
+    def full():
+        z = D.decode_fields(cls, sm, lv)
+        W = D.weights64(cls, inp.gain, inp.scale, z)
+        return D.gemv64(W, inp.x)
+
+    def matvec():
+        return D.gemv64(W0, inp.x)
+
+    def timed(fn, threads, budget, warm):
+        with threadpool_limits(limits=threads):
+            if warm:
+                fn()
+            n, t0 = 0, time.perf_counter()
+            while True:
+                fn()
+                n += 1
+                el = time.perf_counter() - t0
+                if el >= budget or n >= 100000:
+                    break
+        return el / n * 1e6, n
+
+    legs = {}
+    for name, fn in (("decode_and_matvec", full), ("matvec_only", matvec)):
+        for label, threads in (("1_thread", 1), ("all_cores", cores)):
+            us, n = timed(fn, threads, seconds / 4, fn is matvec)
+            legs[f"{name}_{label}"] = {"us_per_gemv": round(us, 1), "threads": threads,
+                                       "repeats": n, "GBps_served_equiv": round(served / us / 1e3, 4)}
+    main = legs["decode_and_matvec_all_cores"]
+    return {"value": main["GBps_served_equiv"], "unit": "GB/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"{n} full {inp.M}x{inp.K} GEMVs on the host (oracle decode_fields + "
-                      f"weights64 + gemv64, f64), {el:.1f} s; GB/s of Planes14 served bytes",
-            "us_per_gemv": el / n * 1e6}
+            "sample": f"full {inp.M}x{inp.K} GEMVs on the host (oracle decode_fields + weights64 + "
+                      f"gemv64, f64; BLAS on {cores} threads), {main['repeats']} repeats; "
+                      f"GB/s of Planes14 served bytes",
+            "us_per_gemv": main["us_per_gemv"], "legs": legs,
+            "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count(), "affinity_cores": cores}
 
 
 def main():
@@ -936,7 +1124,8 @@ def main():
     verified = verify_arms(torch, inp, arms, y_arms)
 
     # warmup every arm (eager, then its graphs), then the contract's timed
-    # region: K Planes14 GEMVs
+    # region: K Planes14 GEMVs from replica 0, after the replay that evicts
+    # them from the Infinity Cache
     k_arm = max(50, args.steps // 4)
     for a in arms.values():
         a.run(args.warmup)
@@ -947,27 +1136,43 @@ def main():
     ms = time_arm(torch, main_arm, args.steps)
     us = ms * 1e3 / args.steps
     gbs = main_arm.served_bytes / (us * 1e-6) / 1e9
+    ev_start, ev_len, between = main_arm.evict_plan(args.steps)
+    n_rep = len(main_arm.launchers)
+    timed = {"timed_bytes": args.steps * main_arm.served_bytes,
+             "working_set_bytes": n_rep * main_arm.served_bytes,
+             "evict_replay": {"first_replica": ev_start, "launches": ev_len,
+                              "bytes": ev_len * main_arm.served_bytes},
+             "timed_replicas_read_by_evict_replay": ev_len == n_rep,
+             "min_bytes_between_reads": between}
+    cyc = cycle_us(torch, main_arm)
+    timed["whole_cycle"] = {"launches": n_rep, "bytes": n_rep * main_arm.served_bytes,
+                            "us_per_gemv": round(cyc, 3),
+                            "GBps": round(main_arm.served_bytes / (cyc * 1e-6) / 1e9, 1)}
+    clock = shader_clock(torch, main_arm)
+    log(f"[bench] timed region {timed}; shader clock {clock}")
+
+    prologue = {f"{inp.M}x{inp.K}": prologue_table(args, torch, P, main_arm)}
+    log(f"[bench] prologue modes {prologue}")
 
     # layout comparison: arms interleaved in fixed order, rounds, first discarded
-    per_round = {n: [] for n in arms}
-    for r in range(args.rounds):
-        for n, a in arms.items():
-            per_round[n].append(time_arm(torch, a, k_arm) * 1e3 / k_arm)
-        log(f"[bench] round {r + 1}/{args.rounds} done")
-    kept = {n: v[args.discard:] for n, v in per_round.items()}
-    table = {}
-    for n, v in kept.items():
-        med = statistics.median(v)
-        row = {"us_per_gemv": round(med, 3), "min_us": round(min(v), 3), "max_us": round(max(v), 3),
-               "served_bytes": arms[n].served_bytes}
-        if arms[n].served_bytes:
-            row["GBps"] = round(arms[n].served_bytes / (med * 1e-6) / 1e9, 1)
-            row["pct_hbm_peak"] = round(100 * row["GBps"] / HBM_PEAK_GBS, 1)
-            row["bits_per_weight"] = round(8 * arms[n].served_bytes / (inp.M * inp.Kpad), 3)
-        if "fp16" in kept:
-            ratios = [f / t for f, t in zip(kept["fp16"], v)]
-            row["vs_fp16"] = round(statistics.median(ratios), 3)
-        table[n] = row
+    table = arms_table(args, torch, arms, inp)
+    table_c4 = None
+    if not args.no_arms_c4 and args.config != "c4_8192x8192":
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        inp4, arms4, y4 = build_arms(args, torch, P, synth, "c4_8192x8192")
+        verify_arms(torch, inp4, arms4, y4)
+        for a in arms4.values():
+            a.run(args.warmup)
+        table_c4 = {"workload": f"single GEMV W {inp4.M}x{inp4.K} (Kpad {inp4.Kpad}), every layout "
+                                f"of the same codes and both controls",
+                    "lane_cols": arms4["planes14"].desc.lane_cols,
+                    "arms": arms_table(args, torch, arms4, inp4)}
+        prologue[f"{inp4.M}x{inp4.K}"] = prologue_table(args, torch, P, arms4["planes14"])
+        log(f"[bench] prologue modes {prologue}")
+        del arms4, y4
+        torch.cuda.empty_cache()
 
     batch = None
     if not args.no_batch:
@@ -1036,11 +1241,16 @@ def main():
                                f"block scales, batch 1", "M": inp.M, "K": inp.K, "Kpad": inp.Kpad,
                    "layout": "planes14", "lane_cols": main_arm.desc.lane_cols,
                    "served_bytes_per_gemv": main_arm.served_bytes,
-                   "replicas": len(main_arm.launchers)},
+                   "replicas": len(main_arm.launchers),
+                   "timed_bytes": timed["timed_bytes"]},
+        "timed_region": timed,
+        "shader_clock": clock,
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.config)},
         "arms": table,
+        "arms_c4": table_c4,
+        "prologue_modes_us": prologue,
         "verified": verified,
         "batch": batch,
         "layer_8b": layer,

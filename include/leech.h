@@ -107,7 +107,11 @@ int leech_codebook_class(const leech_codebook* cb, int class_id, int* shell, int
  *   LEECH_TABLE_INDEX: the format-v1 index table (class offsets and radices,
  *       the codewords by value and by weight, binomial coefficients), read by
  *       leech_transcode_planes14 as d_index_table; exists for the ball
- *       Λ24(12) and smaller balls (N < 2^47). */
+ *       Λ24(12) and smaller balls (N < 2^47).
+ * The per-class magnitudes and the Golay70 value tables are not tables of
+ * their own: the magnitudes are in leech_codebook_class and in bytes 1..5 of
+ * each LEECH_TABLE_DEVICE record, the Golay70 values in its bytes 16..31, so
+ * the kernels read one 32-byte record per class. */
 enum { LEECH_TABLE_CLASS_LEVELS = 0, LEECH_TABLE_CODEWORDS = 1, LEECH_TABLE_DEVICE = 2,
        LEECH_TABLE_INDEX = 3, LEECH_TABLE_GOLAY_GEN = 4 };
 #define LEECH_TABLE_SLOTS 512
@@ -296,6 +300,19 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
 enum { LEECH_EXC_HOISTED = 0, LEECH_EXC_INLINE = 1 };
 int leech_set_exception_mode(int mode);
 
+/* Order in which single (non-batched, non-rotated) GEMVs enqueued from this
+ * call on (process-wide) request their weight records, for measurement (§2.3:
+ * the kernel streams the records; §3.4 attributes the gap to the DRAM floor
+ * largely to latency and occupancy).  Every wave keeps 8 (mode 2: 6) units of
+ * 64 blocks in flight; before the workgroup's staging barrier it requests
+ * all 8 (mode 0), 3 (mode 1) or 2 (mode 2) of them, and the rest one per step
+ * afterwards.  LEECH_PROLOGUE_AUTO (default) picks by the units a wave
+ * streams: ≤ 6 -> 2, ≤ 16 -> 1, more -> 0.  The summation order does not
+ * depend on the mode: y is bit-identical in every mode.  LEECH_E_ARG for
+ * another value. */
+enum { LEECH_PROLOGUE_AUTO = -1 };
+int leech_set_prologue_mode(int mode);
+
 /* GEMV behind the activation rotation in one launch (§2.3: the activation is
  * rotated before the matvec; §6: every consumer rotates): y = W · R(x), where
  * R is leech_rotate_x's blockwise Walsh–Hadamard rotation of the raw binary16
@@ -315,9 +332,13 @@ int leech_gemv_rotated(const leech_layout_desc* desc, const void* d_main, const 
                        const float* group_centroids, int64_t K, const uint16_t* d_x,
                        const int8_t* d_signs, float* d_y, void* stream);
 
-/* Verification decode on the device with the GEMV's own decoders: z int8
- * [M·nb][24], class_id [M·nb], gain_bit [M·nb], row-major (r, j).  Any output
- * may be NULL. */
+/* Verification decode on the device with the GEMV's own decoders (§2.4
+ * "Verification": every block of a served matrix decoded and compared bit for
+ * bit with the reference decode): z int8 [M·nb][24], class_id [M·nb],
+ * gain_bit [M·nb], row-major (r, j).  Any output may be NULL.  LEECH_E_SHAPE
+ * for a descriptor that is not valid, LEECH_E_ARG for a missing stream or
+ * table or a misaligned pointer (d_z and d_main 4-byte, d_side1 8-byte),
+ * LEECH_E_LAYOUT for an unknown layout, LEECH_E_HIP if the launch fails. */
 int leech_decode_blocks(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
                         const void* d_side1, const void* d_class_table,
                         const void* d_codewords, int8_t* d_z, uint16_t* d_class_id,

@@ -14,13 +14,13 @@ from . import _lib
 from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, Codebook,
                    LayoutDesc, LeechError, expand_layout, host_decode_layout, index_decode,
                    index_encode, layout_scales, planes14_desc, set_exception_mode,
-                   EXC_HOISTED, EXC_INLINE)
+                   EXC_HOISTED, EXC_INLINE, set_prologue_mode, PROLOGUE_AUTO)
 
 __all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
            "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
            "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x",
            "index_encode", "index_decode", "planes14_desc", "set_exception_mode",
-           "EXC_HOISTED", "EXC_INLINE"]
+           "EXC_HOISTED", "EXC_INLINE", "set_prologue_mode", "PROLOGUE_AUTO"]
 
 
 def _torch():

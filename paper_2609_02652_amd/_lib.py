@@ -29,7 +29,7 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
            "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch",
-           "leech_gemv_rotated"]
+           "leech_gemv_rotated", "leech_set_prologue_mode"]
 
 
 class LeechError(RuntimeError):
@@ -55,6 +55,14 @@ def _load() -> C.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_2609_02652_amd.build` (no CPU fallback exists)")
+    # The library must resolve its HIP runtime to the one PyTorch loaded, so
+    # that PyTorch's device memory and streams are the library's: loaded the
+    # other way round, the process holds two HIP runtimes and the library's
+    # sees no device.  PyTorch is therefore loaded first when it is installed.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = C.CDLL(LIB_PATH)
     P, I64, U64, I = C.c_void_p, C.c_int64, C.c_uint64, C.c_int
     sig = {
@@ -80,6 +88,7 @@ def _load() -> C.CDLL:
         "leech_planes14_desc": (I, [I64, I64, C.POINTER(LayoutDesc)]),
         "leech_transcode_planes14": (I, [C.POINTER(LayoutDesc), P, P, P, P, P]),
         "leech_set_exception_mode": (I, [I]),
+        "leech_set_prologue_mode": (I, [I]),
         "leech_gemv_batch": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, I, P, I64, P, I64,
                                  P]),
         "leech_gemv_rotated": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, I, P, P, I64, P, P,
@@ -304,3 +313,12 @@ EXC_HOISTED, EXC_INLINE = 0, 1
 def set_exception_mode(mode: int) -> None:
     """Process-wide: how Golay70 GEMVs enqueued afterwards decode exceptions."""
     check(lib.leech_set_exception_mode(mode))
+
+
+PROLOGUE_AUTO = -1
+
+
+def set_prologue_mode(mode: int) -> None:
+    """Process-wide: the order in which single GEMVs enqueued afterwards request
+    their records (PROLOGUE_AUTO, or 0, 1, 2); y does not depend on it."""
+    check(lib.leech_set_prologue_mode(mode))

@@ -50,6 +50,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <type_traits>
 
 #include "leech_internal.h"
 
@@ -63,10 +64,16 @@ typedef uint32_t u32x2a __attribute__((ext_vector_type(2)));
 typedef float f32x4a __attribute__((ext_vector_type(4)));
 
 constexpr int kNoWeights = 99;   // layout id of the no-weights control
-#ifndef LEECH_PREFETCH
-#define LEECH_PREFETCH 8
-#endif
-constexpr int kPrefetch = LEECH_PREFETCH;     // units in flight per wavefront
+// Prologue modes of the GEMV (the host picks one from the units each wave
+// streams, measured per shape): every wave keeps kPrefetch units in flight;
+// the first pro_first(PRO) of them are requested before the staging barrier
+// and the rest one per step of the first round, so that the barrier is not
+// held up behind a burst of record requests that the CU's load path can only
+// accept one after the other.
+//   PRO 0: all 8 before the barrier (long tiles: the deepest early burst);
+//   PRO 1: 3 of 8 before it;   PRO 2: 2 of 6 (waves with ≤ 6 units).
+__host__ __device__ constexpr int pro_prefetch(int pro) { return pro == 2 ? 6 : 8; }
+__host__ __device__ constexpr int pro_first(int pro) { return pro == 0 ? 8 : pro == 1 ? 3 : 2; }
 constexpr float kTwo24 = 16777216.0f;
 // Waves per GEMV workgroup, at most: 8 waves leave each lane up to 256 VGPRs,
 // so the eight prefetch slots and the exception-path decode stay in registers.
@@ -786,8 +793,11 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // (Planes14, NB = 1): blockwise Walsh–Hadamard with the caller's signs, the
 // stages in the order and arithmetic of leech_rotate_x, so the staged binary16
 // activation is bit-identical to that call's output.
-template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false>
+template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false, int PRO = 0>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
+  constexpr int kPrefetch = pro_prefetch(PRO);        // units in flight per wave
+  constexpr int kFirstUnits = pro_first(PRO);         // of them, before the barrier
+  constexpr bool kRamp = kFirstUnits < kPrefetch;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   __shared__ __attribute__((aligned(16))) LdsEntry ts[1024];
   constexpr bool kW = LAYOUT != kNoWeights;
@@ -942,16 +952,22 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   for (int q = 0; q < kXPer; ++q) {
     const bool live = NB == 1 && !ROT && q * nthr + wave * 64 < nb;
     const int off = (tid + q * nthr) * 48;
-    const __amdgpu_buffer_rsrc_t r = live ? rs_x : null_rsrc();
-    xr[q].v0 = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-    xr[q].v1 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
-    xr[q].v2 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 32, 0, 0);
+    if (!live) {      // a wave with no block to stage skips the loads (uniform)
+      xr[q].v0 = xr[q].v1 = xr[q].v2 = u32x4a{0, 0, 0, 0};
+    } else {
+      const __amdgpu_buffer_rsrc_t r = live ? rs_x : null_rsrc();
+      xr[q].v0 = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+      xr[q].v1 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, 0);
+      xr[q].v2 = __builtin_amdgcn_raw_buffer_load_b128(r, off + 32, 0, 0);
+    }
   }
   u32x4a tr = {0, 0, 0, 0}, tr2 = {0, 0, 0, 0}, gr = {0, 0, 0, 0};
   if constexpr (kW) {
+    const bool tlive = wave * 64 < kBallClasses;
     const __amdgpu_buffer_rsrc_t r =
-        wave * 64 < kBallClasses ? make_rsrc(a.table, kBallClasses * sizeof(DevClass)) : null_rsrc();
-    tr = __builtin_amdgcn_raw_buffer_load_b128(r, tid * (int)sizeof(DevClass), 0, 0);
+        tlive ? make_rsrc(a.table, kBallClasses * sizeof(DevClass)) : null_rsrc();
+    if (tlive)
+      tr = __builtin_amdgcn_raw_buffer_load_b128(r, tid * (int)sizeof(DevClass), 0, 0);
     if constexpr (LAYOUT == LEECH_GOLAY70) {
       // the Golay70 value tables (second half of each class record) and the
       // 128-word generator table (wave 0)
@@ -989,11 +1005,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // this wave's full units: wave, wave + waves, ... < gf
   const int units = wave < gf ? (gf - 1 - wave) / waves + 1 : 0;
   Pref pf[kPrefetch];
-#pragma unroll
-  for (int d = 0; d < kPrefetch; ++d) {
-    pf[d] = load_unit<LAYOUT, EVEN>(a, t, d < units, Lp, min(wave + d * waves, g_stand), gside);
+  auto first_load = [&](int d, auto& sd) {
+    pf[d] = load_unit<LAYOUT, EVEN>(a, t, d < units, Lp, min(wave + d * waves, g_stand), sd);
     __builtin_amdgcn_sched_barrier(0);    // keep the slots' loads in slot order
-  }
+  };
+#pragma unroll
+  for (int d = 0; d < kFirstUnits; ++d) first_load(d, gside);
   if constexpr (NB == 1 && !ROT) {
 #pragma unroll
     for (int q = 0; q < kXPer; ++q) {
@@ -1031,6 +1048,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   }
   __syncthreads();
+#pragma unroll
+  for (int d = kFirstUnits; d < kPrefetch; ++d) pf[d] = Pref{0, 0, 0, 0, 0, 0, 0, 0};
 
   auto tab = [&](uint32_t e16) -> LdsEntry {
     return *(const LdsEntry*)__builtin_assume_aligned((const uint8_t*)ts + e16, 16);
@@ -1169,19 +1188,41 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // registers: a refill into fresh registers would be moved back at the loop
   // latch, and moving a register with a load in flight waits for every
   // outstanding load.
-  for (; units - done > kPrefetch; done += kPrefetch) {
+  auto ramp = [&](int d) {     // the first round requests slot d + kFirstUnits
+    if constexpr (kRamp)
+      if (d + kFirstUnits < kPrefetch) first_load(d + kFirstUnits, side);
+  };
+  auto round = [&](auto ramped) {
 #pragma unroll
     for (int d = 0; d < kPrefetch; ++d) {
+      if constexpr (decltype(ramped)::value) ramp(d);
       const int g = wave + (done + d) * waves;
       process(pf[d], g, Lp);
       pf[d] = load_unit<LAYOUT, EVEN>(a, t, done + d + kPrefetch < units, Lp,
                                       min(g + kPrefetch * waves, g_stand), side);
     }
-  }
-  // the last ≤ kPrefetch units are in flight: straight-line, no refills
+  };
+  auto tail = [&](auto ramped) {
+    // the last ≤ kPrefetch units are in flight: straight-line, no refills
 #pragma unroll
-  for (int d = 0; d < kPrefetch; ++d)
-    if (d < units - done) process(pf[d], wave + (done + d) * waves, Lp);
+    for (int d = 0; d < kPrefetch; ++d) {
+      if constexpr (decltype(ramped)::value) ramp(d);
+      if (d < units - done) process(pf[d], wave + (done + d) * waves, Lp);
+    }
+  };
+  if constexpr (kRamp) {
+    if (units > kPrefetch) {
+      round(std::true_type{});
+      done = kPrefetch;
+      for (; units - done > kPrefetch; done += kPrefetch) round(std::false_type{});
+      tail(std::false_type{});
+    } else {
+      tail(std::true_type{});
+    }
+  } else {
+    for (; units - done > kPrefetch; done += kPrefetch) round(std::false_type{});
+    tail(std::false_type{});
+  }
   // the last column group, by the wave next in turn; its lanes past the last
   // column read zero x and add exactly zero
   if (wave == w_last) process(plast, gf, Ll);
@@ -1300,15 +1341,9 @@ static int hip_fail(const char* what, hipError_t e) {
 }
 
 // Waves per workgroup: each wave walks every waves-th unit of the tile.  The
-// summation order depends on it, so it is a function of the shape only (the
-// LEECH_WAVES environment variable overrides the cap, for tuning).
+// summation order depends on it, so it is a function of the shape only.
 static int waves_for(int64_t groups) {
-  static const int cap = [] {
-    const char* v = std::getenv("LEECH_WAVES");
-    const int w = v ? std::atoi(v) : 0;
-    return (w >= 1 && w <= kMaxWaves) ? w : kMaxWaves;
-  }();
-  return (int)std::max<int64_t>(1, std::min<int64_t>(cap, groups));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(kMaxWaves, groups));
 }
 
 static int check_desc_device(const leech_layout_desc* d) {
@@ -1360,26 +1395,52 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
          (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + red;
 }
 
-template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false>
+template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0>
 static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
+  const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO>;
   if (shmem + kTableBytes > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT>), dim3((unsigned)a.tiles),
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO>), dim3((unsigned)a.tiles),
                      dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
   return LEECH_OK;
 }
 
+// Prologue mode of a single GEMV from the most units a wave streams (the
+// tile's full column groups over its waves), by measurement: 4096×4104 (6 a
+// wave) 5.17 -> 4.60 µs with mode 2; 5120×5136 (14) 6.89 -> 6.59 µs with
+// mode 1; 8192×8208 (22) is fastest with mode 0.
+static std::atomic<int> g_pro_mode{LEECH_PROLOGUE_AUTO};
+
+static int prologue_mode(const GemvArgs& a) {
+  const int forced = g_pro_mode.load(std::memory_order_relaxed);
+  if (forced != LEECH_PROLOGUE_AUTO) return forced;
+  const int64_t full = a.groups - 1;
+  const int64_t per_wave = full > 0 ? (full + a.waves - 1) / a.waves : 0;
+  return per_wave <= 6 ? 2 : per_wave <= 16 ? 1 : 0;
+}
+
+template <int LAYOUT, bool EVEN, int NB, int XPER>
+static int launch_gemv_pro(const GemvArgs& a, size_t shmem, hipStream_t st) {
+  if constexpr (NB == 1 && EVEN && LAYOUT != kNoWeights) {
+    switch (prologue_mode(a)) {
+      case 2: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 2>(a, shmem, st);
+      case 1: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 1>(a, shmem, st);
+      default: break;
+    }
+  }
+  return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER>(a, shmem, st);
+}
+
 template <int LAYOUT, bool EVEN, int NB = 1>
 static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
   // one activation block per thread when the workgroup's threads cover them
   if (NB > 1 || a.groups * a.C <= 64 * a.waves)
-    return launch_gemv_kernel<LAYOUT, EVEN, NB, 1>(a, shmem, st);
-  return launch_gemv_kernel<LAYOUT, EVEN, NB, 2>(a, shmem, st);
+    return launch_gemv_pro<LAYOUT, EVEN, NB, 1>(a, shmem, st);
+  return launch_gemv_pro<LAYOUT, EVEN, NB, 2>(a, shmem, st);
 }
 
 
@@ -1669,6 +1730,14 @@ int leech_set_exception_mode(int mode) {
   if (mode != LEECH_EXC_HOISTED && mode != LEECH_EXC_INLINE)
     return set_error(LEECH_E_ARG, "exception mode must be LEECH_EXC_HOISTED or LEECH_EXC_INLINE");
   g_exc_mode.store(mode, std::memory_order_relaxed);
+  return LEECH_OK;
+}
+
+int leech_set_prologue_mode(int mode) {
+  clear_error();
+  if (mode != LEECH_PROLOGUE_AUTO && (mode < 0 || mode > 2))
+    return set_error(LEECH_E_ARG, "prologue mode must be LEECH_PROLOGUE_AUTO, 0, 1 or 2");
+  g_pro_mode.store(mode, std::memory_order_relaxed);
   return LEECH_OK;
 }
 

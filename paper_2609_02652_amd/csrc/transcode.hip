@@ -11,9 +11,10 @@
 // format-v1 routines: a binary search over the class offsets, two or three
 // 64-bit divisions into the mixed-radix digits, colex unranking of each
 // level's positions straight into the three level-code planes, and the
-// record's pair words built from them.  The index
-// table (60 KiB) is read through the caches.  A grid-stride loop bounds the
-// grid; every thread leaves once its slots pass the end of the stream.
+// record's pair words built from them.  Each workgroup first copies the
+// whole index table (60 KiB) into LDS, so the class search, the binomials and
+// the codeword lists are LDS reads.  A grid-stride loop bounds the grid; every
+// thread leaves once its slots pass the end of the stream.
 
 #include <hip/hip_runtime.h>
 
