@@ -235,20 +235,20 @@ def verify_arms(torch, inp, arms, y):
     return res
 
 
-def time_arm(torch, arm, steps):
-    """ms for `steps` GEMVs: one replay of a graph holding exactly `steps`
-    launches (replicas 0, 1, …), bracketed by device synchronisations and
-    timed with HIP events on the stream the kernels run on.  The replay of
-    arm.evict_plan(steps) runs first, outside the timed region, so that the
-    timed replicas are read from HBM."""
-    start, length, _ = arm.evict_plan(steps)
-    if arm.served_bytes:
-        arm.graph(torch, length, start).replay()
-    g = arm.graph(torch, steps)
+def timed_replay(torch, lead, g):
+    """ms of one replay of graph g, timed with HIP events on the current
+    stream.  The device is synchronised first; then `lead` (a graph, or None)
+    is replayed untimed and the events and g are enqueued behind it without
+    waiting, so the device is still busy with `lead` while the host submits
+    g: the timed interval holds g's kernels back to back and not the host's
+    submission of the graph.  The device is synchronised again before the
+    events are read."""
     st = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    if lead is not None:
+        lead.replay()
     e0.record(st)
     g.replay()
     e1.record(st)
@@ -256,22 +256,28 @@ def time_arm(torch, arm, steps):
     return e0.elapsed_time(e1)
 
 
+def time_arm(torch, arm, steps):
+    """ms for `steps` GEMVs: one replay of a graph holding exactly `steps`
+    launches (replicas 0, 1, …), timed with HIP events on the stream the
+    kernels run on, between device synchronisations.  It is enqueued right
+    behind the replay of arm.evict_plan(steps), which streams the replicas
+    the timed region does not read (≥ 512 MiB, twice the Infinity Cache), so
+    that the timed replicas are read from HBM; an arm without weight bytes
+    leads with a replay of its own graph."""
+    g = arm.graph(torch, steps)
+    lead = g
+    if arm.served_bytes:
+        start, length, _ = arm.evict_plan(steps)
+        lead = arm.graph(torch, length, start)
+    return timed_replay(torch, lead, g)
+
+
 def cycle_us(torch, arm, replays=3):
     """µs per GEMV over one whole cycle of the arm's replicas (≥ 1 GiB), median
-    of `replays` timed replays after one untimed one."""
+    of `replays` timed replays, each led by an untimed one."""
     n = len(arm.launchers)
     g = arm.graph(torch, n)
-    g.replay()
-    out = []
-    for _ in range(replays):
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        out.append(e0.elapsed_time(e1) * 1e3 / n)
+    out = [timed_replay(torch, g, g) * 1e3 / n for _ in range(replays)]
     return statistics.median(out)
 
 
@@ -322,15 +328,7 @@ def prologue_table(args, torch, P, arm):
         P.set_prologue_mode(P.PROLOGUE_AUTO)
     for _ in range(5):
         for m, (ev, g) in graphs.items():
-            ev.replay()
-            torch.cuda.synchronize()
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record()
-            g.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            res[m].append(e0.elapsed_time(e1) * 1e3 / k)
+            res[m].append(timed_replay(torch, ev, g) * 1e3 / k)
     del graphs
     return {str(m): round(statistics.median(v), 3) for m, v in res.items()}
 
@@ -498,17 +496,7 @@ def bench_layer(args, torch, P, synth):
         with torch.cuda.graph(g):
             for i in range(steps):
                 fn(i)
-        g.replay()
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        meds = []
-        for _ in range(3):
-            e0.record()
-            g.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            meds.append(e0.elapsed_time(e1) * 1e3 / steps)
+        meds = [timed_replay(torch, g, g) * 1e3 / steps for _ in range(3)]
         res[name] = round(statistics.median(meds), 2)
         log(f"[bench] 8B layer {name}: {res[name]} us/layer ({nrep} replicas)")
         del g
@@ -542,17 +530,7 @@ def replay_us(torch, fn, reps):
     with torch.cuda.graph(g):
         for i in range(reps):
             fn(i)
-    g.replay()
-    torch.cuda.synchronize()
-    meds = []
-    for _ in range(3):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        meds.append(e0.elapsed_time(e1) * 1e3 / reps)
+    meds = [timed_replay(torch, g, g) * 1e3 / reps for _ in range(3)]
     del g
     return statistics.median(meds)
 
@@ -810,17 +788,7 @@ def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
         with torch.cuda.graph(g):
             for _ in range(args.layer_steps):
                 P.rotate_x(x, sg, Kpad, out=out)
-        g.replay()
-        torch.cuda.synchronize()
-        meds = []
-        for _ in range(3):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record()
-            g.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            meds.append(e0.elapsed_time(e1) * 1e3 / args.layer_steps)
+        meds = [timed_replay(torch, g, g) * 1e3 / args.layer_steps for _ in range(3)]
         n = K & -K
         res[f"K{K}"] = {"us": round(statistics.median(meds), 3), "block": n, "workgroups": K // n}
         log(f"[bench] rotation K={K}: {res[f'K{K}']}")
@@ -1003,17 +971,7 @@ def bench_floor(args, torch, P, synth):
         with torch.cuda.graph(g):
             for _ in range(n):
                 fn()
-        g.replay()
-        torch.cuda.synchronize()
-        best = float("inf")
-        for _ in range(5):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record()
-            g.replay()
-            e1.record()
-            torch.cuda.synchronize()
-            best = min(best, e0.elapsed_time(e1) * 1e3 / n)
+        best = min(timed_replay(torch, g, g) * 1e3 / n for _ in range(5))
         del g
         return round(best, 3)
 
