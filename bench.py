@@ -8,13 +8,17 @@ A step is one GEMV y = W x of the workload matrix in the served layout
 HBM.  The timed region is exactly K steps, bracketed by a device
 synchronisation on both sides and timed with HIP events on the launch stream.
 The matrix is held in n replicas (same codes, distinct buffers, ≥ 1 GiB in
-all); step j reads replica j mod n.  Right before the timed replay, a replay
+all); step j reads replica j mod n.  Right before the timed steps, a replay
 of the replicas the timed region does not read (or, when K leaves fewer than
 512 MiB of them, of every replica) streams ≥ 512 MiB, twice the 256 MB
 Infinity Cache, so no replica the timed region reads can still be cached: its
-bytes come from HBM.  The line states the timed bytes, the working set and the
-fewest bytes streamed between a replica's previous read and its timed read,
-and the same GEMV timed over one whole ≥ 1 GiB cycle of replicas beside it.
+bytes come from HBM.  The timed steps are enqueued behind that replay without
+waiting for it: K launches one by one when the host has enqueued them all
+before the device reaches the first (checked, and reported), else one graph
+of K launches; the interval then holds the K kernels back to back.  The line
+states the timed bytes, the working set and the fewest bytes streamed between
+a replica's previous read and its timed read, both launch forms' times, and
+the same GEMV timed over one whole ≥ 1 GiB cycle of replicas beside it.
 
 Printed: one JSON line with the metric (served-weight GB/s of the Planes14
 GEMV), µs per GEMV, the roofline against MI355X's 8 TB/s, every arm of the
@@ -46,7 +50,7 @@ ROT_IN_KERNEL_MAX_TILES = 512
 
 
 def rotate_in_kernel(m, K):
-    tiles = -(-m.desc.M // (64 // m.desc.lane_cols))
+    tiles = -(-m.desc.M // m.desc.tile_rows)
     return K <= ROT_IN_KERNEL_MAX_K and tiles <= ROT_IN_KERNEL_MAX_TILES
 ARMS = ["planes14", "slot32", "planes12x", "planes12x_inline", "golay70", "golay70_inline",
         "fp16", "noweights"]
@@ -88,6 +92,9 @@ def parse():
     ap.add_argument("--no-arms-c4", action="store_true",
                     help="skip the 8192x8192 layout sweep (four layouts, both exception "
                          "decoders, FP16 and no-weights controls)")
+    ap.add_argument("--geometry-sweep", action="store_true",
+                    help="only time the candidate tile geometries of the decoder projection "
+                         "shapes (Planes14) and print them as one JSON line")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -270,6 +277,29 @@ def time_arm(torch, arm, steps):
         start, length, _ = arm.evict_plan(steps)
         lead = arm.graph(torch, length, start)
     return timed_replay(torch, lead, g)
+
+
+def time_arm_stream(torch, arm, steps, leads=2):
+    """ms for `steps` GEMVs launched one by one on the stream (no graph),
+    enqueued behind `leads` replays of the eviction graph of
+    arm.evict_plan(steps), and whether every launch was enqueued before the
+    device reached the timed region (the first event still pending when the
+    host had enqueued the last launch): then the interval holds the kernels
+    back to back, neither the host's launch calls nor a graph's start."""
+    start, length, _ = arm.evict_plan(steps)
+    lead = arm.graph(torch, length, start)
+    st = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    for _ in range(leads):
+        lead.replay()
+    e0.record(st)
+    arm.run(steps)
+    e1.record(st)
+    ahead = not e0.query()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1), ahead
 
 
 def cycle_us(torch, arm, replays=3):
@@ -897,6 +927,95 @@ def bench_large(args, torch, P, synth):
     return res
 
 
+# Decoder projection shapes (rows, Kpad) of the 8B and 14B layers, fused
+# (q/k/v, gate/up) and separate, and the layout sweep's square shape.
+GEOMETRY_SHAPES = [(4096, 4104), (1024, 4104), (6144, 4104), (14336, 4104), (28672, 4104),
+                   (4096, 14352), (5120, 5136), (1024, 5136), (7168, 5136), (17408, 5136),
+                   (34816, 5136), (5120, 17424), (8192, 8208)]
+
+
+def geometry_candidates(M, Kpad, n=6):
+    """The n geometries (lane_cols, tile_rows) of least modelled cost (the
+    library's rule: ceil(tiles / 256) · (units per wave + 3)), plus the
+    power-of-two tile of the same lane_cols."""
+    nb = Kpad // 24
+    cands = []
+    for C in (1, 2, 3, 4, 8, 16):
+        for R in range(4, 64 // C + 1, 4):
+            tiles = -(-M // R)
+            groups = -(-nb // C)
+            waves = min(8, groups)
+            cost = -(-tiles // 256) * (-(-groups // waves) + 3)
+            cands.append((cost, -tiles, -R * C, C, R))
+    cands.sort()
+    out = [(c, r) for *_, c, r in cands[:n]]
+    for C in (1, 2, 4, 8, 16):
+        if (C, 64 // C) not in out and any(c == C for c, _ in out):
+            out.append((C, 64 // C))
+    return out
+
+
+def bench_geometry(args, torch, P, synth):
+    """µs per Planes14 GEMV of each candidate tile geometry on the decoder
+    projection shapes: the measurement behind the library's geometry rule.
+    Codes are drawn once (Planes14's time does not depend on them) and tiled
+    into each shape; every geometry's y is first checked against the library
+    choice's (normalised difference ≤ 2e-3); each timing is a graph replay over
+    ≥ 512 MiB of replicas, geometries interleaved over three rounds, medians."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    dcb = P.DeviceCodebook(P.Codebook(12), dev)
+    pool = synth.make_gemv_inputs(512, 24 * 512, seed=11, name="geometry-pool")
+    pcls, psm, plv = dcb.cb.fields_from_points(pool.z)
+    pcls, psm, plv = pcls.reshape(-1), psm.reshape(-1), plv.reshape(-1, 24)
+    pgain, pscale = pool.gain.reshape(-1), pool.scale.reshape(-1)
+    rng = np.random.default_rng(12)
+    res = {}
+    for M, Kpad in GEOMETRY_SHAPES:
+        t0 = time.time()
+        nb = Kpad // 24
+        pick = rng.integers(0, pcls.size, M * nb)
+        cls, sm = pcls[pick].reshape(M, nb), psm[pick].reshape(M, nb)
+        lv, gain = plv[pick].reshape(M, nb, 24), pgain[pick].reshape(M, nb)
+        scale = pscale[pick].reshape(M, nb)
+        x = torch.from_numpy(synth.make_activation(Kpad, seed=13, name="geometry")).to(dev)
+        y = torch.empty(M, dtype=torch.float32, device=dev)
+        lib = P.layout_geometry(M, Kpad)
+        geos = geometry_candidates(M, Kpad)
+        if lib not in geos:
+            geos.insert(0, lib)
+        mats, yref = {}, None
+        w_norm = torch.from_numpy(np.sqrt((scale.astype(np.float64) ** 2).sum(1))).to(dev)
+        x_norm = float(x.double().norm())
+        for geo in [lib] + [g for g in geos if g != lib]:
+            m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, gain, sm, lv, scale, dev,
+                                           geometry=geo)
+            m0.gemv(x, y)
+            torch.cuda.synchronize()
+            if yref is None:
+                yref = y.clone()
+            d = float(((y - yref).abs().double() / (w_norm * x_norm)).max())
+            if not d <= 2e-3:
+                sys.exit(f"verification failed: geometry {geo} at {M}x{Kpad}: {d:.3g}")
+            reps = max(1, math.ceil((REPLICA_BYTES // 2) / m0.desc.served_bytes))
+            mats[geo] = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0, m0.side1,
+                                              m0.scale.clone(), dcb) for _ in range(reps - 1)]
+        steps = 200 if M * nb < 2_000_000 else 60
+        times = {g: [] for g in mats}
+        for _ in range(3):
+            for g, ms in mats.items():
+                times[g].append(replay_us(torch, lambda i, ms=ms: ms[i % len(ms)].gemv(x, y),
+                                          steps))
+        row = {f"{c}x{r}": round(statistics.median(v), 2) for (c, r), v in times.items()}
+        best = min(row, key=row.get)
+        res[f"{M}x{Kpad}"] = {"library": f"{lib[0]}x{lib[1]}", "best": best, "us": row}
+        log(f"[bench] geometry {M}x{Kpad}: library {lib}, best {best}, {row} "
+            f"({time.time() - t0:.0f}s)")
+        del mats, yref
+        torch.cuda.empty_cache()
+    return res
+
+
 SWEEP = [1024, 2048, 3072, 4096, 6144, 8192, 12288, 16384]
 
 
@@ -1068,6 +1187,9 @@ def main():
     from paper_2609_02652_amd import synth
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU (torch.cuda.is_available() is False)")
+    if args.geometry_sweep:
+        print(json.dumps({"geometry_sweep": bench_geometry(args, torch, P, synth)}), flush=True)
+        return
     if args.calib_mib:
         n = args.calib_mib << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
@@ -1091,12 +1213,20 @@ def main():
     main_arm.graph(torch, args.steps).replay()
     torch.cuda.synchronize()
     log(f"[bench] warmup done; timing {args.steps} planes14 steps")
-    ms = time_arm(torch, main_arm, args.steps)
+    # the K launches one by one behind a lead replay, when the host enqueues
+    # them all before the device reaches them; else one graph of K launches
+    ms_graph = time_arm(torch, main_arm, args.steps)
+    ms_stream, ahead = time_arm_stream(torch, main_arm, args.steps)
+    ms = ms_stream if ahead else ms_graph
     us = ms * 1e3 / args.steps
     gbs = main_arm.served_bytes / (us * 1e-6) / 1e9
     ev_start, ev_len, between = main_arm.evict_plan(args.steps)
     n_rep = len(main_arm.launchers)
-    timed = {"timed_bytes": args.steps * main_arm.served_bytes,
+    timed = {"launch": "stream, enqueued ahead" if ahead else "graph",
+             "us_per_gemv_stream": round(ms_stream * 1e3 / args.steps, 3),
+             "stream_enqueued_ahead": ahead,
+             "us_per_gemv_graph": round(ms_graph * 1e3 / args.steps, 3),
+             "timed_bytes": args.steps * main_arm.served_bytes,
              "working_set_bytes": n_rep * main_arm.served_bytes,
              "evict_replay": {"first_replica": ev_start, "launches": ev_len,
                               "bytes": ev_len * main_arm.served_bytes},

@@ -154,18 +154,27 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *              in-class code per coordinate; blocks the 2-bit code cannot hold
  *              are exceptions as in PLANES12X (§3.2, 3.6 b/w).
  * Records are stored in "wave tile" order: rows are grouped in tiles of
- * tile_rows = 64 / lane_cols rows; within a tile, each run of lane_cols
- * consecutive blocks of the tile's rows forms one 64-block unit, stored row by
- * row.  lane_cols (1, 2, 4, 8 or 16) is chosen from M to even out the CUs'
- * work: the least ceil(tiles / 256) · (tile_rows + 8), ties to fewer tiles
- * (4096 rows: 4; 5120: 2; 8192: 2; 17408: 2; 28672: 1); the kernels read one
- * unit per wavefront step.
+ * tile_rows rows; within a tile, each run of lane_cols consecutive blocks of
+ * the tile's rows forms one unit of tile_rows · lane_cols ≤ 64 blocks, stored
+ * row by row; a tile's units follow each other in column order.  The kernels
+ * read one unit per wavefront step.  The geometry is part of the layout:
+ * lane_cols is 1, 2, 3, 4, 8 or 16 and tile_rows a multiple of 4 with
+ * tile_rows · lane_cols ≤ 64.  leech_expand_layout takes the library's choice
+ * (leech_layout_geometry), which evens out the 256 CUs' work: with
+ * L = ceil(tiles / 256) rounds of one tile per CU and a wave taking every 8th
+ * unit of its tile, the choice has the least
+ * L · 5 + max(L · units per wave, tiles · units per tile / 1664), ties going
+ * to more tiles and then to more blocks per unit (4096 × 4104: 4 × 16, i.e.
+ * lane_cols × tile_rows; 5120 × 5136: 3 × 20; 8192 × 8208: 2 × 32;
+ * 14336 × 4104: 1 × 64).  leech_expand_layout_tiled takes the caller's.
  */
 enum { LEECH_SLOT32 = 0, LEECH_PLANES14 = 1, LEECH_PLANES12X = 2, LEECH_GOLAY70 = 3 };
 
 typedef struct {
   int32_t layout;          /* LEECH_* layout kind                               */
-  int32_t lane_cols;       /* blocks per row in one 64-block unit               */
+  int32_t lane_cols;       /* blocks per row in one unit                        */
+  int32_t tile_rows;       /* rows per tile (and per unit)                      */
+  int32_t reserved;        /* zero                                              */
   int64_t M, Kpad, nb;     /* rows, padded columns, blocks per row              */
   uint64_t main_bytes;     /* bytes of the main record stream (incl. 16-B pad)  */
   uint64_t side_bytes[2];  /* side streams: exception table / per-tile offsets  */
@@ -189,6 +198,21 @@ int leech_expand_layout(const leech_codebook* cb, int layout, int64_t M, int64_t
                         const uint16_t* class_id, const uint8_t* gain_bit,
                         const uint32_t* sign_mask, const uint8_t* level, void* main_out,
                         void* side0_out, void* side1_out, leech_layout_desc* desc);
+
+/* leech_expand_layout with the caller's geometry: lane_cols in {1, 2, 3, 4,
+ * 8, 16} and tile_rows a positive multiple of 4 with tile_rows · lane_cols ≤
+ * 64 (LEECH_E_SHAPE otherwise); lane_cols = tile_rows = 0 takes the library's
+ * choice, as leech_expand_layout does.  Every layout, kernel and entry point
+ * serves every such geometry; the summation order of y depends on it. */
+int leech_expand_layout_tiled(const leech_codebook* cb, int layout, int64_t M, int64_t Kpad,
+                              int32_t lane_cols, int32_t tile_rows, const uint16_t* class_id,
+                              const uint8_t* gain_bit, const uint32_t* sign_mask,
+                              const uint8_t* level, void* main_out, void* side0_out,
+                              void* side1_out, leech_layout_desc* desc);
+
+/* The geometry leech_expand_layout picks for an M × Kpad matrix (the rule
+ * above).  LEECH_E_SHAPE if M ≤ 0, Kpad ≤ 0 or Kpad % 24 != 0. */
+int leech_layout_geometry(int64_t M, int64_t Kpad, int32_t* lane_cols, int32_t* tile_rows);
 
 /* Permute per-block fp16 scales (host, row-major (r, j)) into the layout's
  * wave-tile order; scale_out holds M·nb binary16 values. */
@@ -234,9 +258,11 @@ int leech_index_decode(const leech_codebook* cb, int64_t n, const uint64_t* code
                        uint8_t* level);
 
 /* The Planes14 descriptor of an M × Kpad matrix, without its fields (the
- * layout's size does not depend on the codes): what leech_expand_layout's
- * sizing call returns for LEECH_PLANES14. */
-int leech_planes14_desc(int64_t M, int64_t Kpad, leech_layout_desc* desc);
+ * layout's size does not depend on the codes): what leech_expand_layout_tiled's
+ * sizing call returns for LEECH_PLANES14 and this geometry (lane_cols =
+ * tile_rows = 0: the library's choice). */
+int leech_planes14_desc(int64_t M, int64_t Kpad, int32_t lane_cols, int32_t tile_rows,
+                        leech_layout_desc* desc);
 
 /* --------------------------------------------------------- device calls */
 
@@ -246,8 +272,8 @@ int leech_planes14_desc(int64_t M, int64_t Kpad, leech_layout_desc* desc);
  * LEECH_TABLE_GOLAY_GEN (GOLAY70 only, else may be NULL); d_scale: fp16 scales
  * in wave-tile order (leech_layout_scales); centroid: the two f32 gain
  * centroids; d_x: binary16 [Kpad]; d_y: f32 [M].  Accumulates in f32; the
- * summation order depends only on (M, Kpad, lane_cols), so every layout of
- * one matrix yields bit-identical y. */
+ * summation order depends only on (M, Kpad, lane_cols, tile_rows), so every
+ * layout of one matrix in one geometry yields bit-identical y. */
 int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
                const void* d_side1, const void* d_class_table, const void* d_codewords,
                const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
@@ -270,14 +296,15 @@ int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const vo
                      const uint16_t* d_X, int64_t ldx, float* d_Y, int64_t ldy, void* stream);
 
 /* Row-grouped GEMV (§3.4: q/k/v and gate/up fused into row-concatenated
- * launches): W is the row concatenation of n_groups matrices sharing one
- * activation, expanded as one layout of M = Σ group_rows rows; group g's rows
- * use the gain centroids group_centroids[2g], group_centroids[2g + 1].
- * group_rows and group_centroids are host arrays; every group boundary must
- * be a multiple of 64 rows (so no wave tile straddles two groups).  Other
- * arguments as leech_gemv.  1 ≤ n_groups ≤ LEECH_MAX_GROUPS; LEECH_E_SHAPE if
- * the rows do not sum to M or a boundary is misplaced, LEECH_E_ARG for a
- * non-finite centroid. */
+ * launches, each row with its own matrix's gain centroids): W is the row
+ * concatenation of n_groups matrices sharing one activation, expanded as one
+ * layout of M = Σ group_rows rows; group g's rows use the gain centroids
+ * group_centroids[2g], group_centroids[2g + 1].  group_rows and
+ * group_centroids are host arrays.  A tile may hold rows of two groups (each
+ * lane then reads its own row's centroids), not of three: LEECH_E_SHAPE if a
+ * tile holds two group boundaries other than at its first row, or if the rows
+ * do not sum to M; LEECH_E_ARG for a non-finite centroid.  1 ≤ n_groups ≤
+ * LEECH_MAX_GROUPS.  Other arguments as leech_gemv. */
 #define LEECH_MAX_GROUPS 8
 int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
                        const void* d_side1, const void* d_class_table, const void* d_codewords,

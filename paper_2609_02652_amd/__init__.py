@@ -13,13 +13,14 @@ import numpy as np
 from . import _lib
 from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, Codebook,
                    LayoutDesc, LeechError, expand_layout, host_decode_layout, index_decode,
-                   index_encode, layout_scales, planes14_desc, set_exception_mode,
+                   index_encode, layout_geometry, layout_scales, planes14_desc,
+                   set_exception_mode,
                    EXC_HOISTED, EXC_INLINE, set_prologue_mode, PROLOGUE_AUTO)
 
 __all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
            "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
            "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x",
-           "index_encode", "index_decode", "planes14_desc", "set_exception_mode",
+           "index_encode", "index_decode", "planes14_desc", "layout_geometry", "set_exception_mode",
            "EXC_HOISTED", "EXC_INLINE", "set_prologue_mode", "PROLOGUE_AUTO"]
 
 
@@ -62,8 +63,11 @@ class LeechMatrix:
 
     @classmethod
     def from_fields(cls, dcb: DeviceCodebook, layout: int, class_id, gain, sign_mask, level,
-                    scale_rowmajor, device="cuda"):
-        desc, main, s0, s1 = expand_layout(dcb.cb, layout, class_id, gain, sign_mask, level)
+                    scale_rowmajor, device="cuda", geometry=None):
+        """Expand decoded fields into `layout` (geometry: (lane_cols, tile_rows),
+        or None for the library's choice) and upload the streams."""
+        desc, main, s0, s1 = expand_layout(dcb.cb, layout, class_id, gain, sign_mask, level,
+                                           geometry)
         sc = layout_scales(desc, scale_rowmajor)
         torch = _torch()
         empty = torch.empty(0, dtype=torch.uint8, device=device)

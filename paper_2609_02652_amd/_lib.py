@@ -29,7 +29,8 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
            "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch",
-           "leech_gemv_rotated", "leech_set_prologue_mode"]
+           "leech_gemv_rotated", "leech_set_prologue_mode", "leech_expand_layout_tiled",
+           "leech_layout_geometry"]
 
 
 class LeechError(RuntimeError):
@@ -39,14 +40,16 @@ class LeechError(RuntimeError):
 
 
 class LayoutDesc(C.Structure):
-    _fields_ = [("layout", C.c_int32), ("lane_cols", C.c_int32), ("M", C.c_int64),
+    _fields_ = [("layout", C.c_int32), ("lane_cols", C.c_int32), ("tile_rows", C.c_int32),
+                ("reserved", C.c_int32), ("M", C.c_int64),
                 ("Kpad", C.c_int64), ("nb", C.c_int64), ("main_bytes", C.c_uint64),
                 ("side_bytes", C.c_uint64 * 2), ("n_exceptions", C.c_uint64),
                 ("served_bytes", C.c_uint64)]
 
     def as_dict(self) -> dict:
         return {"layout": LAYOUT_NAMES.get(self.layout, self.layout), "lane_cols": self.lane_cols,
-                "M": self.M, "Kpad": self.Kpad, "nb": self.nb, "main_bytes": self.main_bytes,
+                "tile_rows": self.tile_rows, "M": self.M, "Kpad": self.Kpad, "nb": self.nb,
+                "main_bytes": self.main_bytes,
                 "side_bytes": [self.side_bytes[0], self.side_bytes[1]],
                 "n_exceptions": self.n_exceptions, "served_bytes": self.served_bytes}
 
@@ -64,7 +67,7 @@ def _load() -> C.CDLL:
     except ImportError:
         pass
     lib = C.CDLL(LIB_PATH)
-    P, I64, U64, I = C.c_void_p, C.c_int64, C.c_uint64, C.c_int
+    P, I64, U64, I, I32 = C.c_void_p, C.c_int64, C.c_uint64, C.c_int, C.c_int32
     sig = {
         "leech_last_error": (C.c_char_p, []),
         "leech_codebook_build": (I, [I, C.POINTER(P)]),
@@ -75,6 +78,9 @@ def _load() -> C.CDLL:
         "leech_codebook_table": (I, [P, I, C.POINTER(P), C.POINTER(C.c_size_t)]),
         "leech_fields_from_points": (I, [P, I64, P, P, P, P]),
         "leech_expand_layout": (I, [P, I, I64, I64, P, P, P, P, P, P, P, C.POINTER(LayoutDesc)]),
+        "leech_expand_layout_tiled": (I, [P, I, I64, I64, I32, I32, P, P, P, P, P, P, P,
+                                          C.POINTER(LayoutDesc)]),
+        "leech_layout_geometry": (I, [I64, I64, C.POINTER(I32), C.POINTER(I32)]),
         "leech_layout_scales": (I, [C.POINTER(LayoutDesc), P, P]),
         "leech_host_decode_layout": (I, [P, C.POINTER(LayoutDesc), P, P, P, P, P, P]),
         "leech_gemv": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P, P]),
@@ -85,7 +91,7 @@ def _load() -> C.CDLL:
         "leech_rotate_x": (I, [I64, I64, P, P, P, P, P]),
         "leech_index_encode": (I, [P, I64, P, P, P, P, P]),
         "leech_index_decode": (I, [P, I64, P, P, P, P, P]),
-        "leech_planes14_desc": (I, [I64, I64, C.POINTER(LayoutDesc)]),
+        "leech_planes14_desc": (I, [I64, I64, I32, I32, C.POINTER(LayoutDesc)]),
         "leech_transcode_planes14": (I, [C.POINTER(LayoutDesc), P, P, P, P, P]),
         "leech_set_exception_mode": (I, [I]),
         "leech_set_prologue_mode": (I, [I]),
@@ -195,27 +201,40 @@ def index_decode(cb: Codebook, code):
     return cls.reshape(shp), g.reshape(shp), sm.reshape(shp), lv.reshape(shp + (24,))
 
 
-def planes14_desc(M: int, Kpad: int) -> LayoutDesc:
+def layout_geometry(M: int, Kpad: int) -> tuple:
+    """The library's (lane_cols, tile_rows) for an M × Kpad matrix."""
+    c, r = C.c_int32(), C.c_int32()
+    check(lib.leech_layout_geometry(M, Kpad, C.byref(c), C.byref(r)))
+    return c.value, r.value
+
+
+def planes14_desc(M: int, Kpad: int, geometry=None) -> LayoutDesc:
+    """Planes14 descriptor; geometry = (lane_cols, tile_rows) or None for the
+    library's choice."""
+    lc, tr = geometry or (0, 0)
     d = LayoutDesc()
-    check(lib.leech_planes14_desc(M, Kpad, C.byref(d)))
+    check(lib.leech_planes14_desc(M, Kpad, lc, tr, C.byref(d)))
     return d
 
 
 # ------------------------------------------------------------------- layouts
-def expand_layout(cb: Codebook, layout: int, class_id, gain, sign_mask, level):
-    """Fields (row-major [M, nb]) -> (desc, main, side0, side1) host byte arrays."""
+def expand_layout(cb: Codebook, layout: int, class_id, gain, sign_mask, level, geometry=None):
+    """Fields (row-major [M, nb]) -> (desc, main, side0, side1) host byte arrays;
+    geometry = (lane_cols, tile_rows), or None for the library's choice."""
     class_id = np.ascontiguousarray(class_id, np.uint16)
     gain = np.ascontiguousarray(gain, np.uint8)
     sign_mask = np.ascontiguousarray(sign_mask, np.uint32)
     level = np.ascontiguousarray(level, np.uint8)
     M, nb = class_id.shape
     d = LayoutDesc()
-    args = (cb.handle, layout, M, nb * 24, _ptr(class_id), _ptr(gain), _ptr(sign_mask), _ptr(level))
-    check(lib.leech_expand_layout(*args, None, None, None, C.byref(d)))
+    lc, tr = geometry or (0, 0)
+    args = (cb.handle, layout, M, nb * 24, lc, tr, _ptr(class_id), _ptr(gain), _ptr(sign_mask),
+            _ptr(level))
+    check(lib.leech_expand_layout_tiled(*args, None, None, None, C.byref(d)))
     main = np.zeros(d.main_bytes, np.uint8)
     s0 = np.zeros(max(d.side_bytes[0], 1), np.uint8)
     s1 = np.zeros(max(d.side_bytes[1], 1), np.uint8)
-    check(lib.leech_expand_layout(*args, _ptr(main), _ptr(s0), _ptr(s1), C.byref(d)))
+    check(lib.leech_expand_layout_tiled(*args, _ptr(main), _ptr(s0), _ptr(s1), C.byref(d)))
     return d, main, s0[: d.side_bytes[0]], s1[: d.side_bytes[1]]
 
 

@@ -112,6 +112,7 @@ struct GemvArgs {
   int ngroups;
   int64_t grp_end[LEECH_MAX_GROUPS];      // first row past each group
   float grp_cen[LEECH_MAX_GROUPS][2];
+  int tab2;                     // 1: some tile holds rows of two groups (second LDS table)
   int inline_exc;               // Planes12x, Golay70: 1 = exceptions decoded in the loop
   // batched launches: activation b at x + b·ldx, output b at y + b·ldy, for
   // b < nbatch (≤ the kernel's batch width)
@@ -581,8 +582,18 @@ __device__ __forceinline__ float dot12(const uint32_t h[12], const uint32_t xw[1
 // Sum over the C lanes of a row (C = 1, 2, 4, 8 or 16 adjacent lanes) as an
 // xor butterfly, partners 1, 2, 4, 8 apart in that order: within a quad by DPP
 // quad permutes, across quads by ds_swizzle's xor mode (no address register,
-// no LDS memory).  Every lane is active here.
+// no LDS memory).  For C = 3 the row's first lane adds the next two, fetched
+// by ds_bpermute: (v0 + v1) + v2.  Only the row's first lane (c = 0) holds the
+// row's sum.  Every lane is active here.
 __device__ __forceinline__ float row_sum(float v, int C) {
+  if (C == 3) {
+    const int l = (int)(threadIdx.x & 63u);
+    const float v1 = __builtin_bit_cast(
+        float, __builtin_amdgcn_ds_bpermute(((l + 1) & 63) << 2, __builtin_bit_cast(int, v)));
+    const float v2 = __builtin_bit_cast(
+        float, __builtin_amdgcn_ds_bpermute(((l + 2) & 63) << 2, __builtin_bit_cast(int, v)));
+    return (v + v1) + v2;
+  }
   auto add = [&](int partner) { v += __builtin_bit_cast(float, partner); };
   if (C > 1)
     add(__builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
@@ -762,10 +773,11 @@ __device__ void rotate_activation(const GemvArgs& a, const u32x4a* rx, const u32
 }
 
 // ------------------------------------------------------------------- GEMV
-// LDS: the class table in a static array (entry e at byte e·16 of it, so a
-// decoded field is its own address), then, dynamically sized, x for groups·C
-// block columns (zero past nb), the Golay70 tables, the tile's side data, the
-// cross-wave reduction.
+// LDS, all dynamically sized: the class table (entry e at byte e·16, so a
+// decoded field is its own address; launches whose tiles may hold rows of two
+// row groups keep a second copy, with the second group's centroids, right
+// after it), then x for groups·C block columns (zero past nb), the Golay70
+// tables, the tile's side data, the cross-wave reduction.
 template <int LAYOUT>
 __host__ __device__ constexpr bool has_units() {
   return LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
@@ -799,16 +811,17 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   constexpr int kFirstUnits = pro_first(PRO);         // of them, before the barrier
   constexpr bool kRamp = kFirstUnits < kPrefetch;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-  __shared__ __attribute__((aligned(16))) LdsEntry ts[1024];
   constexpr bool kW = LAYOUT != kNoWeights;
+  LdsEntry* ts = (LdsEntry*)smem;                                  // 1024 (or 2048) entries
+  uint8_t* const xbase = smem + (kW ? (a.tab2 ? 2 * kTableBytes : kTableBytes) : 0);
   constexpr bool kUnits = has_units<LAYOUT>();
   constexpr bool kExc = has_exc<LAYOUT>();
   constexpr uint32_t kExcEntry = LAYOUT == LEECH_PLANES12X ? kP12EntryBytes : kPlanes14Bytes;
   const int64_t nb = a.nb;
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
   const int xblocks = groups * C;
-  uint32_t* xs = (uint32_t*)smem;                                  // NB × xblocks × 12 x pairs
-  uint8_t* p = smem + (size_t)NB * xblocks * 48;
+  uint32_t* xs = (uint32_t*)xbase;                                 // NB × xblocks × 12 x pairs
+  uint8_t* p = xbase + (size_t)NB * xblocks * 48;
   G70Entry* gs = (G70Entry*)p;                                          // Golay70: 301 entries
   uint32_t* cws = (uint32_t*)(p + kG70Entries * sizeof(G70Entry));      // 128 words
   if constexpr (LAYOUT == LEECH_GOLAY70) p += kG70LdsBytes;
@@ -819,7 +832,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   float* pre = (float*)p;                                               // kPreFloats
   if constexpr (kExc) p += kPreFloats * 4;
   const bool red_x = red_in_x(NB, xblocks, waves);
-  float* red = red_x ? (float*)smem : (float*)p;                   // NB × waves × 64
+  float* red = red_x ? (float*)xbase : (float*)p;                  // NB × waves × 64
   float* rb = (float*)p + NB * waves * 64;                         // ROT (NB = 1): rotation buffer
 
   const int tid = threadIdx.x, nthr = blockDim.x;
@@ -905,19 +918,34 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
     }
   }
-  // the tile's gain centroids: its row group's (tiles never straddle groups)
-  float cen0 = a.cen0, cen1 = a.cen1;
+  // the tile's gain centroids: its first row's group's, and where a second
+  // group starts inside the tile (row `split` of it), that group's, staged in
+  // the second table; each lane reads the table of its own row's group
+  float cen0 = a.cen0, cen1 = a.cen1, cen0b = 0.0f, cen1b = 0.0f;
+  bool two = false;
+  int split = R_t;
   if (a.ngroups > 0) {
     const int64_t row0 = (int64_t)tile * a.R;
     int gi = 0;
     while (gi < a.ngroups - 1 && row0 >= a.grp_end[gi]) ++gi;
     cen0 = a.grp_cen[gi][0];
     cen1 = a.grp_cen[gi][1];
+    if (gi < a.ngroups - 1 && a.grp_end[gi] < row0 + R_t) {
+      two = true;
+      split = (int)(a.grp_end[gi] - row0);
+      cen0b = a.grp_cen[gi + 1][0];
+      cen1b = a.grp_cen[gi + 1][1];
+    }
   }
+  const uint32_t toff = two && rl >= split ? (uint32_t)kTableBytes : 0u;
   if constexpr (kW)
     for (int c = tid + nthr; c < kBallClasses; c += nthr) {
       ts[c] = make_entry(a.table, (uint32_t)c, cen0, cen1);
       ts[c + 512] = make_entry(a.table, (uint32_t)c | 512u, cen0, cen1);
+      if (two) {
+        ts[1024 + c] = make_entry(a.table, (uint32_t)c, cen0b, cen1b);
+        ts[1024 + c + 512] = make_entry(a.table, (uint32_t)c | 512u, cen0b, cen1b);
+      }
       if constexpr (LAYOUT == LEECH_GOLAY70) gs[c] = make_g70(a.table, (uint32_t)c);
     }
   const uint8_t* side_units = LAYOUT == LEECH_SLOT32 ? a.side0 : a.side1;
@@ -1030,6 +1058,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       ts[tid] = e;
       e.factor = f * cen1;
       ts[tid + 512] = e;
+      if (two) {
+        e.factor = f * cen0b;
+        ts[1024 + tid] = e;
+        e.factor = f * cen1b;
+        ts[1024 + tid + 512] = e;
+      }
       if constexpr (LAYOUT == LEECH_GOLAY70) gs[tid] = g70_entry(tr, tr2);
     }
     if constexpr (LAYOUT == LEECH_GOLAY70)
@@ -1051,9 +1085,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
   for (int d = kFirstUnits; d < kPrefetch; ++d) pf[d] = Pref{0, 0, 0, 0, 0, 0, 0, 0};
 
-  auto tab = [&](uint32_t e16) -> LdsEntry {
-    return *(const LdsEntry*)__builtin_assume_aligned((const uint8_t*)ts + e16, 16);
+  // the entry of a decoded field for this lane's row, and the entry at a
+  // table byte address (field | table offset)
+  auto tab_at = [&](uint32_t addr) -> LdsEntry {
+    return *(const LdsEntry*)__builtin_assume_aligned(smem + addr, 16);
   };
+  auto tab = [&](uint32_t e16) -> LdsEntry { return tab_at(e16 | toff); };
   auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
   auto cw = [&](uint32_t m) -> uint32_t { return golay_word(cws, m); };
 
@@ -1104,7 +1141,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         for (int k = 0; k < 12; ++k) xw[k] = xj[k];
         uint32_t e16, W[3], h[12];
         p14_record(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, W, e16);
-        const LdsEntry te = tab(e16);
+        // the table of the block's own row (ul / cols of its tile)
+        const LdsEntry te = tab_at(e16 | (two && (int)(ul / cols) >= split ? kTableBytes : 0u));
         p14_core(W, te.tlo, te.thi, h);
         pre[e] = dot12(h, xw) * te.factor;
       }
@@ -1350,11 +1388,11 @@ static int check_desc_device(const leech_layout_desc* d) {
   if (!d) return set_error(LEECH_E_ARG, "desc is NULL");
   if (d->M <= 0 || d->Kpad <= 0 || d->Kpad % kDim || d->nb != d->Kpad / kDim)
     return set_error(LEECH_E_SHAPE, "descriptor shape is not valid");
-  if (d->lane_cols != choose_lane_cols(d->M))
-    return set_error(LEECH_E_SHAPE, "descriptor lane_cols does not match its M");
+  if (!geometry_ok(d->lane_cols, d->tile_rows))
+    return set_error(LEECH_E_SHAPE, "descriptor geometry (lane_cols, tile_rows) is not valid");
   // tile offsets (R·nb·20 bytes at most) and unit counts stay within 31 bits
   if (d->M > (1ll << 31) || d->nb > (1ll << 24) ||
-      (uint64_t)(kWave / d->lane_cols) * (uint64_t)d->nb * 20u > 0x7FFFFFFFull)
+      (uint64_t)d->tile_rows * (uint64_t)d->nb * 20u > 0x7FFFFFFFull)
     return set_error(LEECH_E_SHAPE, "matrix too large for 32-bit tile offsets");
   return LEECH_OK;
 }
@@ -1365,7 +1403,7 @@ static GemvArgs make_args(const leech_layout_desc* d) {
   a.M = d->M;
   a.nb = d->nb;
   a.C = d->lane_cols;
-  a.R = kWave / d->lane_cols;
+  a.R = d->tile_rows;
   a.groups = (d->nb + a.C - 1) / a.C;
   a.waves = waves_for(a.groups);
   a.inline_exc = g_exc_mode.load(std::memory_order_relaxed) == LEECH_EXC_INLINE;
@@ -1377,7 +1415,8 @@ static GemvArgs make_args(const leech_layout_desc* d) {
 }
 
 // Every unit base of a fixed-stride layout is 4-aligned when the last tile's
-// units are (full tiles: 64 blocks per unit and a multiple of 4 rows per tile).
+// units are (tile bases are: tile_rows is a multiple of 4; so are a full
+// tile's unit bases, R · C blocks apart).
 static bool even_bases(const GemvArgs& a, int layout) {
   const int64_t stride = layout == LEECH_PLANES14 ? kPlanes14Bytes
                          : layout == LEECH_PLANES12X ? kPlanes12Bytes
@@ -1389,7 +1428,8 @@ static bool even_bases(const GemvArgs& a, int layout) {
 template <int LAYOUT, int NB = 1>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
   const size_t red = red_in_x(NB, a.groups * a.C, a.waves) ? 0 : (size_t)NB * a.waves * 64 * 4;
-  return (size_t)NB * a.groups * a.C * 48 + (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
+  const size_t table = LAYOUT == kNoWeights ? 0 : (a.tab2 ? 2 : 1) * (size_t)kTableBytes;
+  return table + (size_t)NB * a.groups * a.C * 48 + (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
          (has_exc<LAYOUT>() ? kExcLdsBytes : 0) +
          (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + red;
@@ -1398,7 +1438,7 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
 template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0>
 static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
   const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO>;
-  if (shmem + kTableBytes > 64 * 1024) {
+  if (shmem > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
@@ -1447,7 +1487,7 @@ static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
 template <int LAYOUT, int NB = 1>
 static int launch_gemv(const GemvArgs& a, hipStream_t st) {
   const size_t shmem = gemv_lds_bytes<LAYOUT, NB>(a);
-  if (shmem + kTableBytes > 160 * 1024)
+  if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
   if (LAYOUT == kNoWeights || even_bases(a, LAYOUT))
     return launch_gemv_as<LAYOUT, true, NB>(a, shmem, st);
@@ -1462,7 +1502,7 @@ static size_t rot_lds_bytes(const GemvArgs& a) {
 
 static int launch_gemv_rotated(const GemvArgs& a, hipStream_t st) {
   const size_t shmem = rot_lds_bytes(a);
-  if (shmem + kTableBytes > 160 * 1024)
+  if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "K too large for the LDS-staged rotation");
   if (even_bases(a, LEECH_PLANES14))
     return launch_gemv_kernel<LEECH_PLANES14, true, 1, 1, true>(a, shmem, st);
@@ -1480,7 +1520,7 @@ static int batch_width(const GemvArgs& a, int left) {
                         : w == 8 ? gemv_lds_bytes<LEECH_PLANES14, 8>(a)
                         : w == 4 ? gemv_lds_bytes<LEECH_PLANES14, 4>(a)
                                  : gemv_lds_bytes<LEECH_PLANES14, 2>(a);
-    if (need + kTableBytes <= 160 * 1024) return w;
+    if (need <= 160 * 1024) return w;
   }
   return 1;
 }
@@ -1601,12 +1641,22 @@ static int set_groups(const leech_layout_desc* desc, int n_groups, const int64_t
   if (!group_rows || !group_centroids) return set_error(LEECH_E_ARG, "NULL argument");
   if (n_groups < 1 || n_groups > LEECH_MAX_GROUPS)
     return set_error(LEECH_E_ARG, "n_groups must be 1.." + std::to_string(LEECH_MAX_GROUPS));
-  int64_t end = 0;
+  // a tile holds rows of at most two groups: at most one group boundary
+  // strictly inside it (a boundary on its first row starts it in a new group)
+  int64_t end = 0, straddled = -1;
+  a.tab2 = 0;
   for (int g = 0; g < n_groups; ++g) {
     if (group_rows[g] <= 0) return set_error(LEECH_E_SHAPE, "every group needs rows");
     end += group_rows[g];
-    if (g + 1 < n_groups && end % kWave)
-      return set_error(LEECH_E_SHAPE, "group boundaries must be multiples of 64 rows");
+    if (g + 1 < n_groups && end % a.R) {
+      const int64_t t = end / a.R;
+      if (t == straddled)
+        return set_error(LEECH_E_SHAPE, "a tile of " + std::to_string(a.R) +
+                                            " rows would hold rows of three groups (tile " +
+                                            std::to_string(t) + ")");
+      straddled = t;
+      a.tab2 = 1;
+    }
     const float c0 = group_centroids[2 * g], c1 = group_centroids[2 * g + 1];
     if (!std::isfinite(c0) || !std::isfinite(c1))
       return set_error(LEECH_E_ARG, "group centroids must be finite");

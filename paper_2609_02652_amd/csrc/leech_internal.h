@@ -108,19 +108,20 @@ __host__ __device__ inline int level_code(int level) { return level + 1; }
 static_assert(sizeof(DevClass) == 32, "device class record is 32 bytes");
 
 // Geometry shared by the expansion and the kernels: rows are grouped into
-// tiles of tile_rows = 64 / lane_cols rows; a unit is the 64 (or fewer, at the
-// edges) blocks of one tile × lane_cols consecutive block columns, stored row
-// by row.  Units of a tile are stored in column order; tiles in row order.
+// tiles of R = tile_rows rows; a unit is the R · C (or fewer, at the edges)
+// blocks of one tile × C = lane_cols consecutive block columns, stored row by
+// row, and a wavefront step decodes one unit with lane r · C + c on block
+// (r, c) of it (lanes past R · C hold no block).  Units of a tile are stored in
+// column order; tiles in row order.
 struct Geometry {
   int64_t M, nb;
   int C;            // lane_cols
-  int R;            // tile_rows = 64 / C
+  int R;            // tile_rows
   int64_t tiles;    // ceil(M / R)
   int64_t groups;   // units per tile = ceil(nb / C)
 
-  Geometry(int64_t M_, int64_t nb_, int C_)
-      : M(M_), nb(nb_), C(C_), R(kWave / C_), tiles((M_ + kWave / C_ - 1) / (kWave / C_)),
-        groups((nb_ + C_ - 1) / C_) {}
+  Geometry(int64_t M_, int64_t nb_, int C_, int R_)
+      : M(M_), nb(nb_), C(C_), R(R_), tiles((M_ + R_ - 1) / R_), groups((nb_ + C_ - 1) / C_) {}
   int rows_in_tile(int64_t t) const { return (int)std::min<int64_t>(R, M - t * R); }
   int cols_in_group(int64_t g) const { return (int)std::min<int64_t>(C, nb - g * C); }
   // first block index of unit (t, g) in storage order
@@ -137,7 +138,15 @@ struct Geometry {
   int64_t units() const { return tiles * groups; }
 };
 
-int choose_lane_cols(int64_t M);
+// A geometry the kernels serve: lane_cols 1, 2, 3, 4, 8 or 16 and tile_rows a
+// multiple of 4 with tile_rows · lane_cols ≤ 64 (so every tile starts on a
+// 4-byte boundary of each fixed-stride stream).
+inline bool geometry_ok(int C, int R) {
+  return (C == 1 || C == 2 || C == 3 || C == 4 || C == 8 || C == 16) && R >= 4 && R % 4 == 0 &&
+         R * C <= kWave;
+}
+// The library's geometry for an M × (24 · nb) matrix.
+void choose_geometry(int64_t M, int64_t nb, int* C, int* R);
 
 // thread-local error reporting
 int set_error(int code, const std::string& msg);

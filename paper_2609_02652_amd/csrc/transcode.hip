@@ -139,14 +139,14 @@ extern "C" int leech_transcode_planes14(const leech_layout_desc* desc, const voi
   if (desc->layout != LEECH_PLANES14)
     return set_error(LEECH_E_LAYOUT, "the transcoder writes the Planes14 layout only");
   if (desc->M <= 0 || desc->Kpad <= 0 || desc->Kpad % kDim || desc->nb != desc->Kpad / kDim ||
-      desc->lane_cols != choose_lane_cols(desc->M))
+      !geometry_ok(desc->lane_cols, desc->tile_rows))
     return set_error(LEECH_E_SHAPE, "descriptor shape is not valid");
   const int64_t n = desc->M * desc->nb;
   if (desc->main_bytes != (uint64_t)n * kPlanes14Bytes + kPadBytes)
     return set_error(LEECH_E_SHAPE, "descriptor size is not the Planes14 size of its shape");
   if (((uintptr_t)d_main & 15) || ((uintptr_t)d_code & 7) || ((uintptr_t)d_index_table & 15))
     return set_error(LEECH_E_ARG, "misaligned device pointer");
-  Geometry geo(desc->M, desc->nb, desc->lane_cols);
+  Geometry geo(desc->M, desc->nb, desc->lane_cols, desc->tile_rows);
   TranscodeArgs a;
   a.T = (const IdxTable*)d_index_table;
   a.code = d_code;

@@ -109,9 +109,9 @@ def test_invalid_codes_are_counted_and_zeroed(dev, dcb):
 
 def host_storage_index(desc):
     """Storage slot of block (r, j) in the wave-tile order (rows grouped in
-    tiles of 64 / lane_cols, units of lane_cols columns, stored row by row)."""
+    tiles of tile_rows, units of lane_cols columns, stored row by row)."""
     C = desc.lane_cols
-    R = 64 // C
+    R = desc.tile_rows
     M, nb = desc.M, desc.nb
 
     def index(r, j):

@@ -9,9 +9,10 @@ configuration the benchmark times.
 Each matrix is drawn with its own seed, served as Planes14, decoded on the GPU
 and compared with the drawn points in full (bit-exact), and its GEMV is
 compared with the oracle's f64 matvec on sampled rows, which the oracle
-computes one by one.  These shapes take lane_cols 1, 2, 4 and 16.  A tall matrix
-with an odd-height last tile at lane_cols 1 exercises the kernel variant whose
-unit bases are not 4-aligned, for every layout.
+computes one by one.  These shapes take the geometries (lane_cols × tile_rows)
+1 × 56, 2 × 28, 3 × 20, 4 × 16 and 16 × 4.  A tall matrix with a one-row last
+tile at 1 × 64 exercises the kernel variant whose unit bases are not
+4-aligned, for every layout.
 """
 import sys
 
@@ -53,7 +54,8 @@ def dcb(dev):
     return P.DeviceCodebook(P.Codebook(12), dev)
 
 
-def check_matrix(dev, dcb, name, M, K, seed, layouts=("planes14",), rows_sampled=128):
+def check_matrix(dev, dcb, name, M, K, seed, layouts=("planes14",), rows_sampled=128,
+                 geometry=None):
     inp = synth.make_gemv_inputs(M, K, seed=seed, name=name)
     cls, sm, lv = dcb.cb.fields_from_points(inp.z)
     x = torch.from_numpy(inp.x).to(dev)
@@ -66,7 +68,8 @@ def check_matrix(dev, dcb, name, M, K, seed, layouts=("planes14",), rows_sampled
     ys = {}
     for lay in layouts:
         say(f"[workload] {name} {M}x{K} layout={lay} seed={seed}")
-        mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[lay], cls, inp.gain, sm, lv, inp.scale, dev)
+        mat = P.LeechMatrix.from_fields(dcb, P.LAYOUTS[lay], cls, inp.gain, sm, lv, inp.scale, dev,
+                                        geometry=geometry)
         z, c, g = mat.decode()
         y = mat.gemv(x, centroids=CEN)
         torch.cuda.synchronize()
@@ -74,7 +77,7 @@ def check_matrix(dev, dcb, name, M, K, seed, layouts=("planes14",), rows_sampled
         assert (g.cpu().numpy() == inp.gain).all()
         yh = y.cpu().numpy()
         e = D.errors(yh[rows], y64, W, inp.x)
-        say(f"    lane_cols={mat.desc.lane_cols} errors {e}")
+        say(f"    geometry={mat.desc.lane_cols}x{mat.desc.tile_rows} errors {e}")
         assert e["max_norm_err"] <= TOL_NORM and e["max_abs_err"] <= TOL_PAPER, (name, lay, e)
         ys[lay] = yh
         del mat, z, c, g
@@ -97,10 +100,10 @@ def test_model_14b_shapes(dev, dcb, proj):
 
 
 def test_odd_last_tile_all_layouts(dev, dcb):
-    """lane_cols 1 with a one-row last tile: unit bases that are not 4-aligned."""
-    assert P.planes14_desc(14337, 24 * 5).lane_cols == 1
+    """Geometry 1 × 64 with a one-row last tile: unit bases that are not 4-aligned."""
     check_matrix(dev, dcb, "tall-odd", 14337, 24 * 5, seed=7,
-                 layouts=("planes14", "slot32", "planes12x", "golay70"), rows_sampled=256)
+                 layouts=("planes14", "slot32", "planes12x", "golay70"), rows_sampled=256,
+                 geometry=(1, 64))
 
 
 # ----------------------------------------------------------- fused launches

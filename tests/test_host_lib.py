@@ -116,7 +116,7 @@ def test_record_sizes_and_exceptions(cb):
     d12 = P.expand_layout(cb, P.PLANES12X, cls, inp.gain, sm, lv)[0]
     assert d12.n_exceptions == five
     assert d12.main_bytes == 12 * n + 16 and d12.side_bytes[0] == 16 * five + 16
-    assert d12.side_bytes[1] == 4 * ((256 + 63 // d12.lane_cols) // (64 // d12.lane_cols))
+    assert d12.side_bytes[1] == 4 * -(-256 // d12.tile_rows)
     ds = P.expand_layout(cb, P.SLOT32, cls, inp.gain, sm, lv)[0]
     assert ds.main_bytes == 16 * n + 4 * five + 16
     dg = P.expand_layout(cb, P.GOLAY70, cls, inp.gain, sm, lv)[0]
@@ -202,13 +202,14 @@ def test_grouped_gemv_validates_groups_before_launch():
     launch (the device pointers are stand-ins that are never dereferenced)."""
     d = P.LayoutDesc()
     d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 128, 48, 2
-    d.lane_cols = 16                     # what the library picks for M = 128
+    d.lane_cols, d.tile_rows = 16, 4     # what the library picks for M = 128
     fake = 256
     cases = [
         ([], [], -1),                                 # no group
         ([16] * 8 + [0], [(1, 1)] * 9, -1),           # more than 8 groups
         ([64, 32], [(1, 1), (1, 1)], -3),             # rows do not sum to M
-        ([32, 96], [(1, 1), (1, 1)], -3),             # boundary not on 64 rows
+        ([2, 1, 125], [(1, 1)] * 3, -3),              # tile 0 would hold three groups
+        ([65, 1, 62], [(1, 1)] * 3, -3),              # so would tile 16
         ([64, 64], [(1, float("nan")), (1, 1)], -1),  # non-finite centroid
         ([64, 0, 64], [(1, 1)] * 3, -3),              # empty group
     ]
@@ -223,7 +224,7 @@ def test_batch_gemv_validates_before_launch():
     device pointers, never dereferenced)."""
     d = P.LayoutDesc()
     d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 128, 48, 2
-    d.lane_cols = 16
+    d.lane_cols, d.tile_rows = 16, 4
     fake = 256
     cases = [
         (P.PLANES14, 0, 48, 128, -1),       # empty batch
@@ -242,7 +243,7 @@ def test_batch_gemv_validates_before_launch():
 def test_rotated_gemv_validates_before_launch():
     d = P.LayoutDesc()
     d.layout, d.M, d.Kpad, d.nb = P.PLANES14, 128, 48, 2
-    d.lane_cols = 16
+    d.lane_cols, d.tile_rows = 16, 4
     fake = 256
     cases = [
         (P.PLANES14, 0, -3),          # K = 0
@@ -272,19 +273,44 @@ def test_rotate_validates_before_launch():
     assert e.value.code == -1
 
 
-def test_lane_cols_fill_the_gpu():
-    """lane_cols minimises ceil(tiles / 256) · (rows per tile + 8): 4096 rows
-    take 4 (256 tiles of 16), 5120 rows 2 (160 of 32 rather than 320 of 16),
-    17408 rows 2 (544 of 32 rather than 272 of 64), 28672 rows 1."""
-    from paper_2609_02652_amd._lib import LayoutDesc  # noqa: F401
-    cases = {1: 16, 768: 16, 1024: 16, 2048: 8, 3000: 4, 4096: 4, 5120: 2, 6144: 2, 7168: 2,
-             8192: 2, 14336: 1, 14337: 1, 16384: 1, 17408: 2, 28672: 1, 34816: 2, 152064: 1}
-    for M, C in cases.items():
-        cb_ = P.Codebook(12)
-        inp = synth.make_gemv_inputs(M, 24, seed=0, name="lc")
-        cls, sm, lv = cb_.fields_from_points(inp.z)
-        d = P.expand_layout(cb_, P.PLANES14, cls, inp.gain, sm, lv)[0]
-        assert d.lane_cols == C, M
+def test_geometry_fills_the_gpu():
+    """The library's geometry has the least L · 5 + max(L · units per wave,
+    tiles · units per tile / 1664), L = ceil(tiles / 256), ties to more tiles,
+    then to more blocks per unit: 5120-row projections take 256 tiles of
+    3 × 20 rather than 160 of 2 × 32, the other decoder shapes full 64-block
+    units."""
+    cases = {(1, 24): (1, 64), (64, 24): (16, 4), (768, 1536): (16, 4), (1024, 4104): (16, 4),
+             (4096, 4104): (4, 16), (5120, 5136): (3, 20), (5120, 17424): (3, 20),
+             (6144, 4104): (2, 32), (7168, 5136): (2, 32), (8192, 8208): (2, 32),
+             (14336, 4104): (1, 64), (14337, 120): (1, 60), (17408, 5136): (2, 28),
+             (28672, 4104): (1, 64), (34816, 5136): (2, 32), (16384, 16392): (1, 64),
+             (152064, 5136): (1, 64)}
+    for (M, Kpad), want in cases.items():
+        assert P.layout_geometry(M, Kpad) == want, (M, Kpad)
+    cb_ = P.Codebook(12)
+    inp = synth.make_gemv_inputs(5120, 5136, seed=0, name="geom")
+    cls, sm, lv = cb_.fields_from_points(inp.z)
+    d = P.expand_layout(cb_, P.PLANES14, cls, inp.gain, sm, lv)[0]
+    assert (d.lane_cols, d.tile_rows) == (3, 20)
+    assert (P.planes14_desc(5120, 5136).lane_cols, P.planes14_desc(5120, 5136).tile_rows) == (3, 20)
+
+
+def test_geometry_is_validated(cb):
+    """A caller's geometry must be one the kernels serve: lane_cols in
+    {1, 2, 3, 4, 8, 16}, tile_rows a positive multiple of 4, at most 64 blocks
+    per unit."""
+    inp = synth.make_gemv_inputs(40, 48, seed=0, name="geomv")
+    cls, sm, lv = cb.fields_from_points(inp.z)
+    for geo in ((5, 4), (3, 22), (3, 24), (16, 8), (2, 0), (0, 8), (1, 68)):
+        with pytest.raises(P.LeechError) as e:
+            P.expand_layout(cb, P.PLANES14, cls, inp.gain, sm, lv, geometry=geo)
+        assert e.value.code == -3, geo
+        with pytest.raises(P.LeechError) as e:
+            P.planes14_desc(40, 48, geometry=geo)
+        assert e.value.code == -3, geo
+    for geo in ((3, 20), (1, 64), (16, 4), (2, 12)):
+        d = P.expand_layout(cb, P.PLANES14, cls, inp.gain, sm, lv, geometry=geo)[0]
+        assert (d.lane_cols, d.tile_rows) == geo
 
 
 def test_paper_byte_accounting(cb):
