@@ -145,10 +145,19 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *              0x08070807 is c_a | pos_a << 11 | c_b << 16 | pos_b << 27 for
  *              pair q = 4w + k (k = 0..3; the four rotations cover each bit
  *              of W_w once).
- *   PLANES12X  two bit planes in a 12-byte record for every block; blocks with
- *              five levels also keep their exact PLANES14 record in an exception
- *              table applied in the same launch (§3.2, sub-4.3 b/w): 16-byte
- *              entries, the record plus the block's slot in its tile in bits
+ *   PLANES12X  two bit planes and the sign plane in a 12-byte record for every
+ *              block (§3.2, sub-4.3 b/w), in the GPU's consumption order: bits
+ *              [0, 12) hold the block's table entry, class | gain << 9; the
+ *              other bits hold, for each pair q of the PLANES14 pair list, its
+ *              coordinates' 2-bit levels and non-negative bits at the places
+ *              where one shift or rotation of the record's words leaves them in
+ *              a byte-permute selector (the placement is part of the format and
+ *              listed in the library's sources).  A block with five levels
+ *              keeps its exact PLANES14 record in its tile's exception list,
+ *              applied in the same launch; its record holds only the entry
+ *              field, 1024 + its index in that list (at most 3072 exceptions a
+ *              tile, LEECH_E_CAPACITY otherwise).  Exception entries are 16
+ *              bytes: the record plus the block's slot in its tile in bits
  *              [106, 128).
  *   GOLAY70    9-byte record: class | gain | 12-bit codeword message | a 2-bit
  *              in-class code per coordinate; blocks the 2-bit code cannot hold
@@ -174,7 +183,8 @@ typedef struct {
   int32_t layout;          /* LEECH_* layout kind                               */
   int32_t lane_cols;       /* blocks per row in one unit                        */
   int32_t tile_rows;       /* rows per tile (and per unit)                      */
-  int32_t reserved;        /* zero                                              */
+  uint32_t tile_exc_max;   /* most exception blocks in one tile (PLANES12X,     */
+                           /* GOLAY70; 0 for the other layouts)                 */
   int64_t M, Kpad, nb;     /* rows, padded columns, blocks per row              */
   uint64_t main_bytes;     /* bytes of the main record stream (incl. 16-B pad)  */
   uint64_t side_bytes[2];  /* side streams: exception table / per-tile offsets  */

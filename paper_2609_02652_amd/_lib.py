@@ -41,7 +41,7 @@ class LeechError(RuntimeError):
 
 class LayoutDesc(C.Structure):
     _fields_ = [("layout", C.c_int32), ("lane_cols", C.c_int32), ("tile_rows", C.c_int32),
-                ("reserved", C.c_int32), ("M", C.c_int64),
+                ("tile_exc_max", C.c_uint32), ("M", C.c_int64),
                 ("Kpad", C.c_int64), ("nb", C.c_int64), ("main_bytes", C.c_uint64),
                 ("side_bytes", C.c_uint64 * 2), ("n_exceptions", C.c_uint64),
                 ("served_bytes", C.c_uint64)]

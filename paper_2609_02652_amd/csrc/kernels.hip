@@ -113,6 +113,9 @@ struct GemvArgs {
   int64_t grp_end[LEECH_MAX_GROUPS];      // first row past each group
   float grp_cen[LEECH_MAX_GROUPS][2];
   int tab2;                     // 1: some tile holds rows of two groups (second LDS table)
+  uint32_t tab_bytes;           // bytes of one LDS table copy: 1024 class entries (Planes12x,
+                                // exceptions kept: and the tile's exception entries)
+  uint32_t tile_exc_max;        // most exceptions in one tile
   int inline_exc;               // Planes12x, Golay70: 1 = exceptions decoded in the loop
   // batched launches: activation b at x + b·ldx, output b at y + b·ldy, for
   // b < nbatch (≤ the kernel's batch width)
@@ -187,9 +190,10 @@ __device__ __forceinline__ void LdsSide::exc_window(uint64_t ex, uint32_t w[4], 
 
 // Per-(class, gain) entry staged in LDS at byte (class | gain << 9) · 16.
 struct LdsEntry {
-  uint32_t tlo, thi;    // v_perm table (DevClass::perm)
+  uint32_t tlo, thi;    // v_perm table (DevClass::perm; Planes12x: see p12_core)
   float factor;         // 2^24 · centroid[gain] / (4√m)
-  uint32_t nlev;        // level count
+  uint32_t aux;         // Slot32: level count; Planes12x: f32 added to the block's
+                        // sum × factor (0, or an exception's kept contribution)
 };
 static_assert(sizeof(LdsEntry) * 1024 == kTableBytes, "table entries are 16 bytes");
 // Golay70 per-class entry staged in LDS (index = class id).
@@ -211,6 +215,20 @@ __device__ __forceinline__ uint32_t perm(uint32_t s0, uint32_t s1, uint32_t sel)
 __device__ __forceinline__ uint32_t bfi(uint32_t m, uint32_t a, uint32_t b) {
   uint32_t r;
   asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "s"(m), "v"(a), "v"(b));
+  return r;
+}
+// (s & m) | c as one v_and_or_b32, m from an SGPR and c from a VGPR: left to
+// itself the compiler splits it into a v_and and a v_or with literals (a
+// gfx9 VOP3 instruction takes no literal and one SGPR at most).
+__device__ __forceinline__ uint32_t and_or(uint32_t s, uint32_t m, uint32_t c) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(s), "s"(m), "v"(c));
+  return r;
+}
+// (a << 4) + b as one v_lshl_add_u32.
+__device__ __forceinline__ uint32_t lshl4_add(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_lshl_add_u32 %0, %1, 4, %2" : "=v"(r) : "v"(a), "v"(b));
   return r;
 }
 // Reinterpret a 32-bit word as two binary16 values.  Takes the word by value:
@@ -364,47 +382,66 @@ __device__ __forceinline__ void p14_core(const uint32_t W[3], uint32_t tlo, uint
     }
 }
 
+// Planes12x core: the 12 pair selector words taken straight from the
+// record's words (one funnel shift or rotation each, kP12Sel), each masked to
+// its pair's level and non-negative bits and pointed at the table's
+// magnitude bytes.  The 8-byte table is 0x80 (the binary16 sign byte), three
+// zero bytes, then mags = |z| of levels 0..3: the low half's selector is
+// 4 + level, the high half's 0 (negative: 0x80) or 1, 2 or 8 (0x00).
+__device__ __forceinline__ void p12_core(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t mags,
+                                         uint32_t h[12]) {
+  const uint32_t w[4] = {w0, w1, w2, 0u};
+#pragma unroll
+  for (int q = 0; q < 12; ++q) {
+    const P12Sel d = kP12Sel[q];
+    const uint32_t s = d.rot ? align(w[d.word], w[d.word], d.shift)
+                             : align(w[d.word + 1], w[d.word], d.shift);
+    const uint32_t m = 0x00030003u | 1u << (8 + d.k) | 1u << (24 + d.l);
+    h[q] = perm(mags, 0x80u, and_or(s, m, 0x00040004u));
+  }
+}
+
 // Decode one block into 12 binary16 pairs and its table entry's byte address.
-// tab(e16) returns the LdsEntry at e16 and g70(class) the G70Entry of a class
-// (from LDS in the GEMV, built from the global table in the verification
-// decode); cw(rank) is the Golay codeword of a rank.
-template <int LAYOUT, class TAB, class G70, class CW, class SIDE>
+// tab(e16) returns the LdsEntry at e16 in the layout's own table arrangement
+// and tab14(e16) one whose tlo/thi are the class's Planes14 table (for an
+// exception's exact record); g70(class) the G70Entry of a class (from LDS in
+// the GEMV, built from the global table in the verification decode); cw(rank)
+// is the Golay codeword of a rank.  te receives the entry the block's sum is
+// scaled with.
+template <int LAYOUT, class TAB, class TAB14, class G70, class CW, class SIDE>
 __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int tile, int unit,
-                                             TAB tab, G70 g70, CW cw, const SIDE& side,
-                                             const GemvArgs& a, uint32_t h[12], uint32_t& e16) {
+                                             TAB tab, TAB14 tab14, G70 g70, CW cw,
+                                             const SIDE& side, const GemvArgs& a, uint32_t h[12],
+                                             uint32_t& e16, LdsEntry& te) {
   uint32_t p0 = 0, p1 = 0, p2 = 0, pos = 0;
   // a Planes14 record (the layout's own, or an exception's exact record)
   auto planes14 = [&](uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t sh,
                       uint32_t esh) {
     uint32_t W[3];
     p14_record(w0, w1, w2, w3, sh, esh, W, e16);
-    const LdsEntry t = tab(e16);
-    p14_core(W, t.tlo, t.thi, h);
+    te = tab14(e16);
+    p14_core(W, te.tlo, te.thi, h);
   };
   if constexpr (LAYOUT == LEECH_PLANES14) {
     planes14(p.w0, p.w1, p.w2, p.w3, p.sh, p.esh);
     return;
   } else if constexpr (LAYOUT == LEECH_PLANES12X) {
-    const uint32_t field = p.w2 >> kP12ExcShift;
-    if (field) {      // five-level block: exact Planes14 record from the tile's list
-      const uint64_t ex = (uint64_t)(side.p12_base(tile) + field - 1);
+    const uint32_t ent = p.w0 & 0xFFFu;
+    if (ent >= kP12ExcEntry0) {   // five-level block: exact Planes14 record from the tile's list
+      const uint64_t ex = (uint64_t)(side.p12_base(tile) + ent - kP12ExcEntry0);
       uint32_t w[4], sh;
       side.template exc_window<kP12EntryBytes>(ex, w, sh);
       planes14(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u);
-      return;
     } else {
-      // two-plane level (0..3) -> code planes of level + 1, bit-parallel
-      e16 = (p.w0 << 4) & 0x3FF0u;
-      pos = ~align(p.w1, p.w0, 10);
-      const uint32_t l0 = p.w1 >> 2, l1 = align(p.w2, p.w1, 26);
-      p0 = ~l0;
-      p1 = l0 ^ l1;
-      p2 = l0 & l1;
+      e16 = ent << 4;
+      te = tab(e16);
+      p12_core(p.w0, p.w1, p.w2, te.thi, h);
     }
+    return;
   } else if constexpr (LAYOUT == LEECH_SLOT32) {
     // one-hot masks of levels 1..4 -> code planes of level + 1 (codes 1..5)
     e16 = (p.w0 << 4) & 0x3FF0u;
-    const uint32_t L = tab(e16).nlev;
+    const uint32_t L = tab(e16).aux;
     pos = ~align(p.w1, p.w0, 10);
     const uint32_t m1 = L > 1 ? p.w1 >> 2 : 0u;
     const uint32_t m2 = L > 2 ? align(p.w2, p.w1, 26) : 0u;
@@ -428,11 +465,12 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
       e16 = (r0 << 4) & 0x3FF0u;
       const uint32_t side_bits = cw((r0 >> 10) & 0xFFFu);
       golay70_core(align(r1, r0, 22), align(r2, r1, 14), side_bits, g70((e16 >> 4) & 511u), h);
+      te = tab(e16);
       return;
     }
   }
-  const LdsEntry t = tab(e16);
-  planes_core(p0, p1, p2, pos, t.tlo, t.thi, h);
+  te = tab(e16);
+  planes_core(p0, p1, p2, pos, te.tlo, te.thi, h);
 }
 
 // Per-workgroup view of the streams: buffer descriptors based at the tile's
@@ -511,7 +549,34 @@ __device__ __forceinline__ LdsEntry make_entry(const DevClass* tab, uint32_t e, 
   t.tlo = d.x;
   t.thi = d.y;
   t.factor = __builtin_bit_cast(float, (uint32_t)d.z) * kTwo24 * ((e >> 9) ? cen1 : cen0);
-  t.nlev = d.w & 0xFFu;
+  t.aux = d.w & 0xFFu;
+  return t;
+}
+
+// Planes12x entries: tlo holds the Planes14 table's high word (|z| of
+// levels 3 and 4), thi the magnitudes p12_core reads (levels 0..3), aux the
+// added term (0 for a class).  p12_as14 rebuilds the Planes14 table, for an
+// exception's exact record.
+__device__ __forceinline__ LdsEntry p12_entry(uint32_t tlo14, uint32_t thi14, float factor) {
+  LdsEntry t;
+  t.tlo = thi14;
+  t.thi = align(thi14, tlo14, 8);
+  t.factor = factor;
+  t.aux = 0u;
+  return t;
+}
+__device__ __forceinline__ LdsEntry p12_as14(const LdsEntry& t) {
+  LdsEntry r = t;
+  r.tlo = t.thi << 8 | 0x80u;
+  r.thi = t.tlo;
+  return r;
+}
+// The entry in a layout's own arrangement.
+template <int LAYOUT>
+__device__ __forceinline__ LdsEntry make_entry_as(const DevClass* tab, uint32_t e, float cen0,
+                                                  float cen1) {
+  LdsEntry t = make_entry(tab, e, cen0, cen1);
+  if constexpr (LAYOUT == LEECH_PLANES12X) t = p12_entry(t.tlo, t.thi, t.factor);
   return t;
 }
 
@@ -812,10 +877,13 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   constexpr bool kRamp = kFirstUnits < kPrefetch;
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   constexpr bool kW = LAYOUT != kNoWeights;
-  LdsEntry* ts = (LdsEntry*)smem;                                  // 1024 (or 2048) entries
-  uint8_t* const xbase = smem + (kW ? (a.tab2 ? 2 * kTableBytes : kTableBytes) : 0);
+  LdsEntry* ts = (LdsEntry*)smem;                    // one table copy, or two
+  uint8_t* const xbase = smem + (kW ? (a.tab2 ? 2 : 1) * a.tab_bytes : 0);
   constexpr bool kUnits = has_units<LAYOUT>();
   constexpr bool kExc = has_exc<LAYOUT>();
+  // Golay70 stages its tile's exception records in LDS and keeps their
+  // contributions in `pre`; Planes12x keeps them as table entries
+  constexpr bool kExcLds = LAYOUT == LEECH_GOLAY70;
   constexpr uint32_t kExcEntry = LAYOUT == LEECH_PLANES12X ? kP12EntryBytes : kPlanes14Bytes;
   const int64_t nb = a.nb;
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
@@ -828,9 +896,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   uint8_t* units_lds = p;                                               // groups × 16 B
   if constexpr (kUnits) p += (size_t)groups * kUnitEntryBytes;
   uint8_t* exc_lds = p;                                                 // ≤ kExcLdsBytes
-  if constexpr (kExc) p += kExcLdsBytes;
+  if constexpr (kExcLds) p += kExcLdsBytes;
   float* pre = (float*)p;                                               // kPreFloats
-  if constexpr (kExc) p += kPreFloats * 4;
+  if constexpr (kExcLds) p += kPreFloats * 4;
   const bool red_x = red_in_x(NB, xblocks, waves);
   float* red = red_x ? (float*)xbase : (float*)p;                  // NB × waves × 64
   float* rb = (float*)p + NB * waves * 64;                         // ROT (NB = 1): rotation buffer
@@ -891,7 +959,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     side.exc_start = (e0 * kExcEntry) & ~15ull;
     const uint64_t end = e1 * kExcEntry + (kExcEntry == kPlanes14Bytes ? 2 : 0);
     exc_chunks = (end - side.exc_start + 15) / 16;
-    side.exc_in_lds = exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
+    side.exc_in_lds = kExcLds && exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
     exc_first = (uint32_t)e0;
     exc_count = (uint32_t)(e1 - e0);
   }
@@ -937,14 +1005,15 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       cen1b = a.grp_cen[gi + 1][1];
     }
   }
-  const uint32_t toff = two && rl >= split ? (uint32_t)kTableBytes : 0u;
+  const uint32_t toff = two && rl >= split ? a.tab_bytes : 0u;
   if constexpr (kW)
     for (int c = tid + nthr; c < kBallClasses; c += nthr) {
-      ts[c] = make_entry(a.table, (uint32_t)c, cen0, cen1);
-      ts[c + 512] = make_entry(a.table, (uint32_t)c | 512u, cen0, cen1);
+      ts[c] = make_entry_as<LAYOUT>(a.table, (uint32_t)c, cen0, cen1);
+      ts[c + 512] = make_entry_as<LAYOUT>(a.table, (uint32_t)c | 512u, cen0, cen1);
       if (two) {
-        ts[1024 + c] = make_entry(a.table, (uint32_t)c, cen0b, cen1b);
-        ts[1024 + c + 512] = make_entry(a.table, (uint32_t)c | 512u, cen0b, cen1b);
+        LdsEntry* t2 = (LdsEntry*)(smem + a.tab_bytes);
+        t2[c] = make_entry_as<LAYOUT>(a.table, (uint32_t)c, cen0b, cen1b);
+        t2[c + 512] = make_entry_as<LAYOUT>(a.table, (uint32_t)c | 512u, cen0b, cen1b);
       }
       if constexpr (LAYOUT == LEECH_GOLAY70) gs[c] = make_g70(a.table, (uint32_t)c);
     }
@@ -952,7 +1021,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if constexpr (kUnits)
     for (int u = tid + kUPer * nthr; u < groups; u += nthr)
       ((u32x4a*)units_lds)[u] = ((const u32x4a*)side_units)[tile * groups + u];
-  if constexpr (kExc)
+  if constexpr (kExcLds)
     if (side.exc_in_lds)
       for (int64_t c = tid + (int64_t)kEPer * nthr; c < (int64_t)exc_chunks; c += nthr)
         ((u32x4a*)exc_lds)[c] = ((const u32x4a*)(a.side0 + side.exc_start))[c];
@@ -1019,7 +1088,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   }
   if constexpr (kExc) {
-    const uint64_t n_chunks = side.exc_in_lds ? exc_chunks : 0;
+    // Planes12x: the tile's exception entries, for the hoisted decoder
+    const uint64_t n_chunks =
+        (kExcLds ? side.exc_in_lds : !a.inline_exc) ? exc_chunks : 0;
     const __amdgpu_buffer_rsrc_t re = make_rsrc(a.side0 + side.exc_start, n_chunks * 16);
 #pragma unroll
     for (int q = 0; q < kEPer; ++q) {
@@ -1052,17 +1123,19 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       LdsEntry e;
       e.tlo = tr.x;
       e.thi = tr.y;
-      e.nlev = tr.w & 0xFFu;
+      e.aux = tr.w & 0xFFu;
+      if constexpr (LAYOUT == LEECH_PLANES12X) e = p12_entry(tr.x, tr.y, 0.0f);
       const float f = __builtin_bit_cast(float, (uint32_t)tr.z) * kTwo24;
       e.factor = f * cen0;
       ts[tid] = e;
       e.factor = f * cen1;
       ts[tid + 512] = e;
       if (two) {
+        LdsEntry* t2 = (LdsEntry*)(smem + a.tab_bytes);
         e.factor = f * cen0b;
-        ts[1024 + tid] = e;
+        t2[tid] = e;
         e.factor = f * cen1b;
-        ts[1024 + tid + 512] = e;
+        t2[tid + 512] = e;
       }
       if constexpr (LAYOUT == LEECH_GOLAY70) gs[tid] = g70_entry(tr, tr2);
     }
@@ -1074,7 +1147,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     for (int q = 0; q < kUPer; ++q)
       if (tid + q * nthr < groups) ((u32x4a*)units_lds)[tid + q * nthr] = ur[q];
   }
-  if constexpr (kExc) {
+  if constexpr (kExcLds) {
     if (side.exc_in_lds) {
 #pragma unroll
       for (int q = 0; q < kEPer; ++q)
@@ -1085,12 +1158,20 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
   for (int d = kFirstUnits; d < kPrefetch; ++d) pf[d] = Pref{0, 0, 0, 0, 0, 0, 0, 0};
 
-  // the entry of a decoded field for this lane's row, and the entry at a
-  // table byte address (field | table offset)
+  // the entry of a decoded field for this lane's row (the first table copy, or
+  // the second at toff), in the layout's arrangement and as a Planes14 table,
+  // and the entry at a table byte address
   auto tab_at = [&](uint32_t addr) -> LdsEntry {
     return *(const LdsEntry*)__builtin_assume_aligned(smem + addr, 16);
   };
-  auto tab = [&](uint32_t e16) -> LdsEntry { return tab_at(e16 | toff); };
+  auto tab = [&](uint32_t e16) -> LdsEntry {
+    // a power-of-two copy size lets the offset be or'ed into the field's mask
+    return tab_at(LAYOUT == LEECH_PLANES12X ? e16 + toff : e16 | toff);
+  };
+  auto tab14 = [&](uint32_t e16) -> LdsEntry {
+    if constexpr (LAYOUT == LEECH_PLANES12X) return p12_as14(tab(e16));
+    else return tab(e16);
+  };
   auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
   auto cw = [&](uint32_t m) -> uint32_t { return golay_word(cws, m); };
 
@@ -1101,7 +1182,45 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // an exception takes the kept value in place of its own.  Same products,
   // same order: y is unchanged.
   bool hoisted = false;
-  if constexpr (kExc) {
+  if constexpr (LAYOUT == LEECH_PLANES12X) {
+    // Planes12x: each exception gets a table entry of its own, at the entry
+    // number its record holds (in its row's table copy): no magnitudes, so the
+    // loop's lookups give zeros and its sum is +0, and the exception's
+    // contribution dot12 · factor as the added term, so the loop's
+    // fma(sum, factor, added) gives that contribution exactly.
+    hoisted = !a.inline_exc;
+    if (hoisted) {
+      auto keep = [&](uint32_t e, const u32x4a& w) {
+        // the entry names the block's slot in the tile; units are R_t × C
+        // blocks in column order
+        const uint32_t slot = w.w >> (kP12PosShift - 96);
+        const int unit = min((int)(slot / (uint32_t)(R_t * C)), gf);
+        const uint32_t ul = slot - (uint32_t)(unit * R_t * C);
+        const uint32_t cols = unit == gf ? (uint32_t)C_last : (uint32_t)C;
+        const uint32_t* xj = xs + 12 * (unit * C + ul % cols);
+        uint32_t xw[12];
+#pragma unroll
+        for (int k = 0; k < 12; ++k) xw[k] = xj[k];
+        uint32_t e16, W[3], h[12];
+        p14_record(w.x, w.y, w.z, w.w, 0u, 28u, W, e16);
+        const uint32_t off = two && (int)(ul / cols) >= split ? a.tab_bytes : 0u;
+        const LdsEntry te = p12_as14(tab_at(e16 + off));
+        p14_core(W, te.tlo, te.thi, h);
+        LdsEntry k;
+        k.tlo = 0u;
+        k.thi = 0u;
+        k.factor = 0.0f;
+        k.aux = __builtin_bit_cast(uint32_t, dot12(h, xw) * te.factor);
+        *(LdsEntry*)(smem + ((kP12ExcEntry0 + e) << 4) + off) = k;
+      };
+#pragma unroll
+      for (int q = 0; q < kEPer; ++q)
+        if (tid + q * nthr < (int)exc_count) keep(tid + q * nthr, er[q]);
+      for (uint32_t e = tid + kEPer * nthr; e < exc_count; e += nthr)
+        keep(e, *(const u32x4a*)(a.side0 + (uint64_t)(exc_first + e) * kP12EntryBytes));
+      __syncthreads();
+    }
+  } else if constexpr (kExc) {
     hoisted = !a.inline_exc && side.exc_in_lds;
     if (hoisted) {
       for (uint32_t e = tid; e < exc_count; e += nthr) {
@@ -1110,13 +1229,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         side.template exc_window<kExcEntry>(ex, w, sh);
         int unit;
         uint32_t ul;
-        if constexpr (LAYOUT == LEECH_PLANES12X) {
-          // the entry names the block's slot in the tile; units are R_t × C
-          // blocks in column order
-          const uint32_t slot = w[3] >> (kP12PosShift - 96);
-          unit = min((int)(slot / (uint32_t)(R_t * C)), gf);
-          ul = slot - (uint32_t)(unit * R_t * C);
-        } else {
+        {
           // its unit: the last one whose first exception index is ≤ ex
           int lo = 0, hi = groups - 1;
           while (lo < hi) {
@@ -1142,7 +1255,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         uint32_t e16, W[3], h[12];
         p14_record(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, W, e16);
         // the table of the block's own row (ul / cols of its tile)
-        const LdsEntry te = tab_at(e16 | (two && (int)(ul / cols) >= split ? kTableBytes : 0u));
+        const LdsEntry te = tab_at(e16 | (two && (int)(ul / cols) >= split ? a.tab_bytes : 0u));
         p14_core(W, te.tlo, te.thi, h);
         pre[e] = dot12(h, xw) * te.factor;
       }
@@ -1155,8 +1268,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   float acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = 0.0f;
-  // One unit: decode slot p for unit g and accumulate.
-  auto process = [&](const Pref& pr, int g, const Lane& L) {
+  // One unit: decode slot p for unit g and accumulate.  LAST: the last
+  // column group, whose stand-in lanes (past the last column) must add zero.
+  auto process = [&](const Pref& pr, int g, const Lane& L, auto last) {
     const u32x4a* xp = (const u32x4a*)(x_lane + g * (C * 48));
     const u32x4a x0 = xp[0], x1 = xp[1], x2 = xp[2];
     const uint32_t xw[12] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w,
@@ -1170,17 +1284,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       uint32_t h[12], e16;
       if constexpr (LAYOUT == LEECH_PLANES12X) {
         if (hoisted) {
-          // two-plane level (0..3) -> code planes of level + 1, bit-parallel
-          e16 = (pr.w0 << 4) & 0x3FF0u;
-          const uint32_t pos = ~align(pr.w1, pr.w0, 10);
-          const uint32_t l0 = pr.w1 >> 2, l1 = align(pr.w2, pr.w1, 26);
-          const LdsEntry te = tab(e16);
-          planes_core(~l0, l0 ^ l1, l0 & l1, pos, te.tlo, te.thi, h);
-          float v = dot12(h, xw) * te.factor;
-          // the record's field is 1 + the block's index in the tile's list
-          const uint32_t field = pr.w2 >> kP12ExcShift;
-          const float kept = pre[min(field - 1u, exc_count)];
-          v = field && L.own ? kept : v;
+          // the record's entry field addresses the class's entry or the
+          // exception's own (added term = its kept contribution)
+          const LdsEntry te = tab_at(lshl4_add(pr.w0 & 0xFFFu, toff));
+          p12_core(pr.w0, pr.w1, pr.w2, te.thi, h);
+          float v = __builtin_fmaf(dot12(h, xw), te.factor, __builtin_bit_cast(float, te.aux));
+          if constexpr (decltype(last)::value) v = L.own ? v : 0.0f;
           acc[0] = __builtin_fmaf((float)as_half(pr.scale), v, acc[0]);
           return;
         }
@@ -1206,8 +1315,10 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
           return;
         }
       }
-      decode_block<LAYOUT>(pr, L.ul, tile, tile * groups + g, tab, g70, cw, side, a, h, e16);
-      const float sc = (float)as_half(pr.scale), f = tab(e16).factor;
+      LdsEntry te;
+      decode_block<LAYOUT>(pr, L.ul, tile, tile * groups + g, tab, tab14, g70, cw, side, a, h,
+                           e16, te);
+      const float sc = (float)as_half(pr.scale), f = te.factor;
       acc[0] = __builtin_fmaf(sc, dot12(h, xw) * f, acc[0]);
 #pragma unroll
       for (int b = 1; b < NB; ++b) {
@@ -1235,7 +1346,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     for (int d = 0; d < kPrefetch; ++d) {
       if constexpr (decltype(ramped)::value) ramp(d);
       const int g = wave + (done + d) * waves;
-      process(pf[d], g, Lp);
+      process(pf[d], g, Lp, std::false_type{});
       pf[d] = load_unit<LAYOUT, EVEN>(a, t, done + d + kPrefetch < units, Lp,
                                       min(g + kPrefetch * waves, g_stand), side);
     }
@@ -1245,7 +1356,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
     for (int d = 0; d < kPrefetch; ++d) {
       if constexpr (decltype(ramped)::value) ramp(d);
-      if (d < units - done) process(pf[d], wave + (done + d) * waves, Lp);
+      if (d < units - done) process(pf[d], wave + (done + d) * waves, Lp, std::false_type{});
     }
   };
   if constexpr (kRamp) {
@@ -1263,7 +1374,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   }
   // the last column group, by the wave next in turn; its lanes past the last
   // column read zero x and add exactly zero
-  if (wave == w_last) process(plast, gf, Ll);
+  if (wave == w_last) process(plast, gf, Ll, std::true_type{});
   if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -1315,11 +1426,16 @@ __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, u
     p.sh = (uint32_t)(off & 3u) * 8u;
     p.esh = (p.sh + 28u) & 31u;
   }
-  auto tab = [&](uint32_t e16) -> LdsEntry { return make_entry(a.table, e16 >> 4, 1.0f, 1.0f); };
+  auto tab = [&](uint32_t e16) -> LdsEntry {
+    return make_entry_as<LAYOUT>(a.table, e16 >> 4, 1.0f, 1.0f);
+  };
+  auto tab14 = [&](uint32_t e16) -> LdsEntry { return make_entry(a.table, e16 >> 4, 1.0f, 1.0f); };
   auto g70 = [&](uint32_t c) -> G70Entry { return make_g70(a.table, c); };
   auto cw = [&](uint32_t m) -> uint32_t { return golay_word(a.codewords, m); };
   uint32_t h[12], e16;
-  decode_block<LAYOUT>(p, ul, tile, tile * (int)a.groups + g, tab, g70, cw, side, a, h, e16);
+  LdsEntry te;
+  decode_block<LAYOUT>(p, ul, tile, tile * (int)a.groups + g, tab, tab14, g70, cw, side, a, h,
+                       e16, te);
   int8_t z[kDim];
 #pragma unroll
   for (int k = 0; k < 12; ++k) {
@@ -1411,6 +1527,8 @@ static GemvArgs make_args(const leech_layout_desc* d) {
   a.n_exc = d->n_exceptions;
   a.main_bytes = d->main_bytes;
   a.nbatch = 1;
+  a.tab_bytes = kTableBytes;
+  a.tile_exc_max = d->tile_exc_max;
   return a;
 }
 
@@ -1428,11 +1546,10 @@ static bool even_bases(const GemvArgs& a, int layout) {
 template <int LAYOUT, int NB = 1>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
   const size_t red = red_in_x(NB, a.groups * a.C, a.waves) ? 0 : (size_t)NB * a.waves * 64 * 4;
-  const size_t table = LAYOUT == kNoWeights ? 0 : (a.tab2 ? 2 : 1) * (size_t)kTableBytes;
+  const size_t table = LAYOUT == kNoWeights ? 0 : (a.tab2 ? 2 : 1) * (size_t)a.tab_bytes;
   return table + (size_t)NB * a.groups * a.C * 48 + (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
-         (has_exc<LAYOUT>() ? kExcLdsBytes : 0) +
-         (has_exc<LAYOUT>() ? kPreFloats * 4 : 0) + red;
+         (LAYOUT == LEECH_GOLAY70 ? kExcLdsBytes + kPreFloats * 4 : 0) + red;
 }
 
 template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0>
@@ -1485,7 +1602,20 @@ static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
 
 
 template <int LAYOUT, int NB = 1>
-static int launch_gemv(const GemvArgs& a, hipStream_t st) {
+static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
+  GemvArgs a = a0;
+  if constexpr (LAYOUT == LEECH_PLANES12X) {
+    // the hoisted decoder keeps the tile's exceptions as table entries after
+    // the 1024 class entries; where they do not fit in LDS, exceptions are
+    // decoded in the loop
+    if (!a.inline_exc) {
+      a.tab_bytes = (uint32_t)(kP12ExcEntry0 + a.tile_exc_max) * (uint32_t)sizeof(LdsEntry);
+      if (gemv_lds_bytes<LAYOUT, NB>(a) > 160 * 1024) {
+        a.inline_exc = 1;
+        a.tab_bytes = kTableBytes;
+      }
+    }
+  }
   const size_t shmem = gemv_lds_bytes<LAYOUT, NB>(a);
   if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");

@@ -77,15 +77,56 @@ constexpr int kSlot32Small = 16;     // ≤ 4 levels
 constexpr int kSlot32Large = 20;     // 5 levels
 constexpr int kUnitEntryBytes = 16;  // per-unit side entry: u64 bitmap, u32 base, u32 zero
 
-// Planes12x: the spare bits [82, 96) of the 12-byte record hold 1 + the
-// block's index in its tile's exception list, or 0.  An exception entry is 16
-// bytes: the block's exact Planes14 record (14 bytes, bits [106, 112) zero)
-// with the block's storage slot inside its tile in bits [106, 128).
+// Planes12x record (96 bits, little-endian from its first byte, words W0, W1,
+// W2): bits [0, 12) hold the block's table entry, class | gain << 9, or, for a
+// block with five levels, kP12ExcEntry0 + its index in its tile's exception
+// list; the other 84 bits hold the 12 pairs of coordinates in the GEMV's
+// consumption order, each as one selector word taken straight from the
+// record.  Pair q's selector word is (kP12Sel[q]): word w rotated right by s
+// (rot = 1), or words w + 1 : w shifted right by s (rot = 0); its bits 0, 1
+// hold the level of coordinate kPairCoords[q][0] (bit 0 the low bit), bit
+// 8 + k that coordinate's non-negative bit, bits 16, 17 and 24 + l the same
+// of kPairCoords[q][1].  Bits of the record no selector names are zero.  A
+// five-level block carries only its entry field; its exact Planes14 record is
+// in the exception list.  An exception entry is 16 bytes: the block's exact
+// Planes14 record (14 bytes, bits [106, 112) zero) with the block's storage
+// slot inside its tile in bits [106, 128).
+struct P12Sel {
+  int rot, word, shift, k, l;
+};
+constexpr P12Sel kP12Sel[12] = {{0, 0, 12, 0, 0}, {0, 0, 14, 0, 0}, {0, 0, 16, 0, 0},
+                                {0, 0, 18, 0, 1}, {1, 1, 12, 0, 1}, {1, 1, 14, 0, 1},
+                                {0, 1, 9, 0, 0},  {0, 1, 18, 1, 0}, {0, 1, 23, 1, 1},
+                                {1, 2, 11, 0, 1}, {1, 2, 5, 0, 0},  {1, 2, 14, 1, 3}};
+// Record bit of bit j (0..31) of pair q's selector word.
+__host__ __device__ constexpr int p12_bit(int q, int j) {
+  return kP12Sel[q].rot ? 32 * kP12Sel[q].word + (j + kP12Sel[q].shift) % 32
+                        : 32 * kP12Sel[q].word + kP12Sel[q].shift + j;
+}
+// The six record bits of pair q: level bits 0, 1 and the non-negative bit of
+// its first coordinate, then of its second.
+__host__ __device__ constexpr int p12_pair_bit(int q, int t) {
+  return p12_bit(q, t == 0 ? 0 : t == 1 ? 1 : t == 2 ? 8 + kP12Sel[q].k : t == 3 ? 16
+                    : t == 4 ? 17 : 24 + kP12Sel[q].l);
+}
+// Every pair bit is a distinct record bit outside the entry field.
+__host__ __device__ constexpr bool p12_layout_ok() {
+  for (int q = 0; q < 12; ++q)
+    for (int t = 0; t < 6; ++t) {
+      const int b = p12_pair_bit(q, t);
+      if (b < 12 || b >= 96) return false;
+      for (int q2 = 0; q2 < 12; ++q2)
+        for (int t2 = 0; t2 < 6; ++t2)
+          if ((q2 != q || t2 != t) && p12_pair_bit(q2, t2) == b) return false;
+    }
+  return true;
+}
+static_assert(p12_layout_ok(), "Planes12x pair selectors overlap");
 constexpr int kP12EntryBytes = 16;
 constexpr int kP12PosShift = 106;
 constexpr int kP12PosBits = 22;
-constexpr int kP12ExcShift = 82 - 64;          // bit position inside word 2
-constexpr uint32_t kP12ExcMax = (1u << 14) - 2; // largest storable local index
+constexpr uint32_t kP12ExcEntry0 = 1024;        // entry of a tile's first exception
+constexpr uint32_t kP12ExcMax = 4096 - 1024;    // exceptions one tile may hold
 
 // Device class record: 32 bytes per class id (LEECH_DEVICE_TABLE_BYTES / 512).
 //   perm[8]   : byte table read by v_perm_b32: perm[0] = 0x80 (the binary16
