@@ -159,9 +159,16 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  *              tile, LEECH_E_CAPACITY otherwise).  Exception entries are 16
  *              bytes: the record plus the block's slot in its tile in bits
  *              [106, 128).
- *   GOLAY70    9-byte record: class | gain | 12-bit codeword message | a 2-bit
- *              in-class code per coordinate; blocks the 2-bit code cannot hold
- *              are exceptions as in PLANES12X (§3.2, 3.6 b/w).
+ *   GOLAY70    9-byte record (§3.2, 3.6 b/w): bits [0, 12) the table entry
+ *              (class | gain << 9), [12, 24) the 12-bit message of the block's
+ *              codeword, [24, 48) and [48, 72) the low and high bits of a 2-bit
+ *              in-class code per coordinate (bit i = coordinate i).  A block
+ *              the 2-bit codes cannot hold is an exception as in PLANES12X:
+ *              its record holds only the entry field, 1024 + its index in its
+ *              tile's exception list.
+ * PLANES12X and GOLAY70 keep their exception lists in side0 (the 16-byte
+ * entries, tile after tile) and the index of each tile's first entry in side1
+ * (a u32 per tile).
  * Records are stored in "wave tile" order: rows are grouped in tiles of
  * tile_rows rows; within a tile, each run of lane_cols consecutive blocks of
  * the tile's rows forms one unit of tile_rows · lane_cols ≤ 64 blocks, stored

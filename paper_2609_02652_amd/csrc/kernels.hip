@@ -78,10 +78,8 @@ constexpr float kTwo24 = 16777216.0f;
 // Waves per GEMV workgroup, at most: 8 waves leave each lane up to 256 VGPRs,
 // so the eight prefetch slots and the exception-path decode stay in registers.
 constexpr int kMaxWaves = 8;
-constexpr int kExcLdsBytes = 32 * 1024;   // a tile's exception records staged in LDS
-// Golay70, hoisted: the f32 contribution (block sum × factor) of each of a
-// tile's exceptions, plus one spare slot
-constexpr int kPreFloats = kExcLdsBytes / kPlanes14Bytes + 2;
+// Exception entries a thread holds in registers from the prologue
+constexpr int kExcPrefetch = 4;
 constexpr int kTableBytes = 1024 * 16;    // LDS class-table entries (class | gain << 9)
 // Raw buffer descriptor, word 3, for the gfx9 family (32-bit elements, no
 // swizzle); loads carry the non-temporal hint: records and scales are read once.
@@ -131,10 +129,13 @@ struct GemvArgs {
 };
 
 // Where side data comes from: global memory (verification decode, and the
-// GEMV prologue before LDS is written), or the tile's copy in LDS.
+// GEMV prologue before LDS is written), or the tile's copy in LDS.  Slot32
+// reads its per-unit side entries (record offsets); Planes12x and Golay70 their
+// tiles' exception lists (a u32 first index per tile in side1, 16-byte entries
+// in side0).
 struct GlobalSide {
   const GemvArgs* a;
-  __device__ __forceinline__ uint32_t p12_base(int tile) const {
+  __device__ __forceinline__ uint32_t exc_base(int tile) const {
     return ((const uint32_t*)a->side1)[tile];
   }
   __device__ __forceinline__ void unit_entry(const uint8_t* side, int unit, uint64_t& bits,
@@ -143,66 +144,40 @@ struct GlobalSide {
     bits = *(const uint64_t*)ent;
     base = *(const uint32_t*)(ent + 8);
   }
-  // four-word window holding exception record ex (exact Planes14 record) in a
-  // list of ES-byte entries
-  template <uint32_t ES>
-  __device__ __forceinline__ void exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const;
+  // exception entry ex: the exact Planes14 record in its first 14 bytes
+  __device__ __forceinline__ u32x4a exc_entry(uint64_t ex) const {
+    return *(const u32x4a*)(a->side0 + ex * kExcEntryBytes);
+  }
 };
 struct LdsSide {
   const GemvArgs* a;
-  const uint8_t* exc;        // LDS copy of exception bytes from global offset exc_start
-  uint64_t exc_start;
-  bool exc_in_lds;           // false: the tile's records exceed the LDS budget
-  const uint8_t* units;      // LDS copy of the tile's unit entries
+  const uint8_t* units;      // LDS copy of the tile's unit entries (Slot32)
   int unit0;                 // first unit id of the tile
-  uint32_t p12base;          // Planes12x: first exception index of the tile
-  __device__ __forceinline__ uint32_t p12_base(int) const { return p12base; }
+  uint32_t excbase;          // first exception index of the tile
+  __device__ __forceinline__ uint32_t exc_base(int) const { return excbase; }
   __device__ __forceinline__ void unit_entry(const uint8_t*, int unit, uint64_t& bits,
                                              uint32_t& base) const {
     const uint8_t* ent = units + (unit - unit0) * kUnitEntryBytes;
     bits = *(const uint64_t*)ent;
     base = *(const uint32_t*)(ent + 8);
   }
-  template <uint32_t ES>
-  __device__ __forceinline__ void exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const;
-};
-
-template <uint32_t ES>
-__device__ __forceinline__ void GlobalSide::exc_window(uint64_t ex, uint32_t w[4],
-                                                      uint32_t& sh) const {
-  const uint64_t off = ex * ES;
-  const uint32_t* p = (const uint32_t*)(a->side0 + (off & ~3ull));
-  w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
-  sh = (uint32_t)(off & 2) * 8u;
-}
-template <uint32_t ES>
-__device__ __forceinline__ void LdsSide::exc_window(uint64_t ex, uint32_t w[4], uint32_t& sh) const {
-  const uint64_t goff = ex * ES;
-  if (exc_in_lds) {
-    const uint32_t* p = (const uint32_t*)(exc + ((uint32_t)(goff - exc_start) & ~3u));
-    w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
-  } else {
-    const uint32_t* p = (const uint32_t*)(a->side0 + (goff & ~3ull));
-    w[0] = p[0]; w[1] = p[1]; w[2] = p[2]; w[3] = p[3];
+  __device__ __forceinline__ u32x4a exc_entry(uint64_t ex) const {
+    return *(const u32x4a*)(a->side0 + ex * kExcEntryBytes);
   }
-  sh = (uint32_t)(goff & 2) * 8u;
-}
+};
 
 // Per-(class, gain) entry staged in LDS at byte (class | gain << 9) · 16.
 struct LdsEntry {
-  uint32_t tlo, thi;    // v_perm table (DevClass::perm; Planes12x: see p12_core)
+  uint32_t tlo, thi;    // v_perm table (DevClass::perm; Planes12x: see p12_core;
+                        // Golay70: see golay70_core)
   float factor;         // 2^24 · centroid[gain] / (4√m)
-  uint32_t aux;         // Slot32: level count; Planes12x: f32 added to the block's
-                        // sum × factor (0, or an exception's kept contribution)
+  uint32_t aux;         // Slot32: level count; Planes12x, Golay70: f32 added to the
+                        // block's sum × factor (0, or an exception's kept contribution)
 };
 static_assert(sizeof(LdsEntry) * 1024 == kTableBytes, "table entries are 16 bytes");
-// Golay70 per-class entry staged in LDS (index = class id).
-struct G70Entry {
-  uint32_t alo, ahi;    // |value| at side·4 + code
-  uint32_t slo, shi;    // 0x80 where that value is negative
-};
-constexpr int kG70Entries = 304;    // the ball's 301 classes, rounded to 16
-constexpr int kG70LdsBytes = kG70Entries * 16 + 128 * 4;   // entries + generator table
+// Golay70 in LDS: the generator table, and each class's Planes14 table (for
+// an exception's exact record)
+constexpr int kG70LdsBytes = 128 * 4 + 512 * 8;
 
 __device__ __forceinline__ uint32_t align(uint32_t hi, uint32_t lo, uint32_t s) {
   return __builtin_amdgcn_alignbit(hi, lo, s);
@@ -292,10 +267,13 @@ __device__ __forceinline__ void planes_core(uint32_t p0, uint32_t p1, uint32_t p
   nibble_core(n, tlo, thi, h);
 }
 
-// Golay70 core: nibble (c0, c1, side, 0) -> index side·4 + code; the low half
-// is |value| from one 8-byte table, the high half its sign byte from another.
+// Golay70 core: nibble (c0, c1, side, 0) -> index j = side·4 + code of a
+// coordinate; the class's 8-byte table holds T[j] = |value| | (value < 0) << 7.
+// pair_sources puts each coordinate's nibble in two adjacent selector bytes,
+// so one byte permute gives T[j] in both bytes of its binary16 half, and the
+// mask 0x807F807F keeps the magnitude in the low byte and the sign in the high.
 __device__ __forceinline__ void golay70_core(uint32_t c0, uint32_t c1, uint32_t side,
-                                             const G70Entry& t, uint32_t h[12]) {
+                                             uint32_t tlo, uint32_t thi, uint32_t h[12]) {
   uint32_t n[4];
   nibble_transpose(c0, c1, side, 0u, n);
 #pragma unroll
@@ -303,11 +281,15 @@ __device__ __forceinline__ void golay70_core(uint32_t c0, uint32_t c1, uint32_t 
     uint32_t s[3];
     pair_sources(n[r], s);
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
-      const uint32_t sel = s[k] & 0x07070707u;
-      h[3 * r + k] = bfi(0xFF00FF00u, perm(t.shi, t.slo, sel), perm(t.ahi, t.alo, sel));
-    }
+    for (int k = 0; k < 3; ++k)
+      h[3 * r + k] = perm(thi, tlo, s[k] & 0x07070707u) & 0x807F807Fu;
   }
+}
+// The Golay70 table of a class from the second half of its device record
+// (signed values and magnitudes at side·4 + code).
+__device__ __forceinline__ void g70_table(const u32x4a& v, uint32_t& tlo, uint32_t& thi) {
+  tlo = (uint32_t)v.z | ((uint32_t)v.x & 0x80808080u);
+  thi = (uint32_t)v.w | ((uint32_t)v.y & 0x80808080u);
 }
 
 // Coordinates of pair k of h[] (and of the staged x pairs).
@@ -404,15 +386,12 @@ __device__ __forceinline__ void p12_core(uint32_t w0, uint32_t w1, uint32_t w2, 
 // Decode one block into 12 binary16 pairs and its table entry's byte address.
 // tab(e16) returns the LdsEntry at e16 in the layout's own table arrangement
 // and tab14(e16) one whose tlo/thi are the class's Planes14 table (for an
-// exception's exact record); g70(class) the G70Entry of a class (from LDS in
-// the GEMV, built from the global table in the verification decode); cw(rank)
-// is the Golay codeword of a rank.  te receives the entry the block's sum is
-// scaled with.
-template <int LAYOUT, class TAB, class TAB14, class G70, class CW, class SIDE>
-__device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int tile, int unit,
-                                             TAB tab, TAB14 tab14, G70 g70, CW cw,
-                                             const SIDE& side, const GemvArgs& a, uint32_t h[12],
-                                             uint32_t& e16, LdsEntry& te) {
+// exception's exact record); cw(message) is the Golay codeword of a message.
+// te receives the entry the block's sum is scaled with.
+template <int LAYOUT, class TAB, class TAB14, class CW, class SIDE>
+__device__ __forceinline__ void decode_block(const Pref& p, int tile, TAB tab, TAB14 tab14, CW cw,
+                                             const SIDE& side, uint32_t h[12], uint32_t& e16,
+                                             LdsEntry& te) {
   uint32_t p0 = 0, p1 = 0, p2 = 0, pos = 0;
   // a Planes14 record (the layout's own, or an exception's exact record)
   auto planes14 = [&](uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t sh,
@@ -422,16 +401,19 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
     te = tab14(e16);
     p14_core(W, te.tlo, te.thi, h);
   };
+  // an exception of Planes12x or Golay70: the exact Planes14 record of entry
+  // ent of the tile's list
+  auto exception = [&](uint32_t ent) {
+    const u32x4a w = side.exc_entry((uint64_t)side.exc_base(tile) + ent - kExcEntry0);
+    planes14(w.x, w.y, w.z, w.w, 0u, 28u);
+  };
   if constexpr (LAYOUT == LEECH_PLANES14) {
     planes14(p.w0, p.w1, p.w2, p.w3, p.sh, p.esh);
     return;
   } else if constexpr (LAYOUT == LEECH_PLANES12X) {
     const uint32_t ent = p.w0 & 0xFFFu;
-    if (ent >= kP12ExcEntry0) {   // five-level block: exact Planes14 record from the tile's list
-      const uint64_t ex = (uint64_t)(side.p12_base(tile) + ent - kP12ExcEntry0);
-      uint32_t w[4], sh;
-      side.template exc_window<kP12EntryBytes>(ex, w, sh);
-      planes14(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u);
+    if (ent >= kExcEntry0) {
+      exception(ent);
     } else {
       e16 = ent << 4;
       te = tab(e16);
@@ -452,22 +434,16 @@ __device__ __forceinline__ void decode_block(const Pref& p, uint32_t ul, int til
     p2 = m3 | m4;
   } else if constexpr (LAYOUT == LEECH_GOLAY70) {
     const uint32_t r0 = align(p.w1, p.w0, p.sh), r1 = align(p.w2, p.w1, p.sh), r2 = p.w2 >> p.sh;
-    if ((r2 >> 6) & 1u) {   // exception: exact Planes14 record located by the unit entry
-      uint64_t bits;
-      uint32_t base;
-      side.unit_entry(a.side1, unit, bits, base);
-      const uint64_t ex = base + (uint32_t)__builtin_popcountll(bits & ((1ull << ul) - 1ull));
-      uint32_t w[4], sh;
-      side.template exc_window<kPlanes14Bytes>(ex, w, sh);
-      planes14(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u);
-      return;
+    const uint32_t ent = r0 & 0xFFFu;
+    if (ent >= kExcEntry0) {
+      exception(ent);
     } else {
-      e16 = (r0 << 4) & 0x3FF0u;
-      const uint32_t side_bits = cw((r0 >> 10) & 0xFFFu);
-      golay70_core(align(r1, r0, 22), align(r2, r1, 14), side_bits, g70((e16 >> 4) & 511u), h);
+      e16 = ent << 4;
       te = tab(e16);
-      return;
+      golay70_core(align(r1, r0, kG70C0Pos), align(r2, r1, kG70C1Pos - 32),
+                   cw(r0 >> kG70MsgPos & 0xFFFu), te.tlo, te.thi, h);
     }
+    return;
   }
   te = tab(e16);
   planes_core(p0, p1, p2, pos, te.tlo, te.thi, h);
@@ -577,27 +553,11 @@ __device__ __forceinline__ LdsEntry make_entry_as(const DevClass* tab, uint32_t 
                                                   float cen1) {
   LdsEntry t = make_entry(tab, e, cen0, cen1);
   if constexpr (LAYOUT == LEECH_PLANES12X) t = p12_entry(t.tlo, t.thi, t.factor);
-  return t;
-}
-
-// G70Entry of a class from the two halves of its 32-byte table record.
-__device__ __forceinline__ G70Entry g70_entry(const u32x4a& d, const u32x4a& v) {
-  G70Entry t;
-  t.alo = v.z;
-  t.ahi = v.w;
-  const uint32_t sg = (uint32_t)d.w >> 24;
-  uint32_t slo = 0, shi = 0;
-  for (int k = 0; k < 4; ++k) {
-    slo |= ((sg >> k) & 1u) << (8 * k + 7);
-    shi |= ((sg >> (k + 4)) & 1u) << (8 * k + 7);
+  if constexpr (LAYOUT == LEECH_GOLAY70) {
+    g70_table(*((const u32x4a*)&tab[e & 511u] + 1), t.tlo, t.thi);
+    t.aux = 0u;
   }
-  t.slo = slo;
-  t.shi = shi;
   return t;
-}
-
-__device__ __forceinline__ G70Entry make_g70(const DevClass* tab, uint32_t c) {
-  return g70_entry(*(const u32x4a*)&tab[c], *((const u32x4a*)&tab[c] + 1));
 }
 
 // Golay codeword of a 12-bit message from the 128-entry generator table.
@@ -845,7 +805,7 @@ __device__ void rotate_activation(const GemvArgs& a, const u32x4a* rx, const u32
 // tables, the tile's side data, the cross-wave reduction.
 template <int LAYOUT>
 __host__ __device__ constexpr bool has_units() {
-  return LAYOUT == LEECH_SLOT32 || LAYOUT == LEECH_GOLAY70;
+  return LAYOUT == LEECH_SLOT32;
 }
 template <int LAYOUT>
 __host__ __device__ constexpr bool has_exc() {
@@ -881,24 +841,16 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   uint8_t* const xbase = smem + (kW ? (a.tab2 ? 2 : 1) * a.tab_bytes : 0);
   constexpr bool kUnits = has_units<LAYOUT>();
   constexpr bool kExc = has_exc<LAYOUT>();
-  // Golay70 stages its tile's exception records in LDS and keeps their
-  // contributions in `pre`; Planes12x keeps them as table entries
-  constexpr bool kExcLds = LAYOUT == LEECH_GOLAY70;
-  constexpr uint32_t kExcEntry = LAYOUT == LEECH_PLANES12X ? kP12EntryBytes : kPlanes14Bytes;
   const int64_t nb = a.nb;
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
   const int xblocks = groups * C;
   uint32_t* xs = (uint32_t*)xbase;                                 // NB × xblocks × 12 x pairs
   uint8_t* p = xbase + (size_t)NB * xblocks * 48;
-  G70Entry* gs = (G70Entry*)p;                                          // Golay70: 301 entries
-  uint32_t* cws = (uint32_t*)(p + kG70Entries * sizeof(G70Entry));      // 128 words
+  uint32_t* cws = (uint32_t*)p;                                    // Golay70: 128 words
+  u32x2a* p14t = (u32x2a*)(p + 128 * 4);                           // Golay70: 512 tables
   if constexpr (LAYOUT == LEECH_GOLAY70) p += kG70LdsBytes;
-  uint8_t* units_lds = p;                                               // groups × 16 B
+  uint8_t* units_lds = p;                                          // groups × 16 B
   if constexpr (kUnits) p += (size_t)groups * kUnitEntryBytes;
-  uint8_t* exc_lds = p;                                                 // ≤ kExcLdsBytes
-  if constexpr (kExcLds) p += kExcLdsBytes;
-  float* pre = (float*)p;                                               // kPreFloats
-  if constexpr (kExcLds) p += kPreFloats * 4;
   const bool red_x = red_in_x(NB, xblocks, waves);
   float* red = red_x ? (float*)xbase : (float*)p;                  // NB × waves × 64
   float* rb = (float*)p + NB * waves * 64;                         // ROT (NB = 1): rotation buffer
@@ -932,34 +884,15 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   t.C = C;
   t.groups = groups;
 
-  // Side data of the tile: its unit entries (Slot32, Golay70) and the range of
-  // its exception records (Planes12x, Golay70), copied to LDS below.
+  // Side data of the tile: its unit entries (Slot32, copied to LDS below) and
+  // the range of its exception entries (Planes12x, Golay70).
   const GlobalSide gside{&a};
-  LdsSide side{&a, exc_lds, 0, false, units_lds, tile * groups, 0u};
-  uint64_t exc_chunks = 0;
-  uint32_t exc_first = 0, exc_count = 0;    // the tile's exception records
+  LdsSide side{&a, units_lds, tile * groups, 0u};
+  uint32_t exc_first = 0, exc_count = 0;    // the tile's exception entries
   if constexpr (kExc) {
-    uint64_t e0, e1;
-    if constexpr (LAYOUT == LEECH_PLANES12X) {
-      e0 = ((const uint32_t*)a.side1)[tile];
-      e1 = tile + 1 < a.tiles ? ((const uint32_t*)a.side1)[tile + 1] : a.n_exc;
-      side.p12base = (uint32_t)e0;
-    } else {
-      uint64_t bits;
-      uint32_t b0, b1 = 0;
-      gside.unit_entry(a.side1, tile * groups, bits, b0);
-      if (tile + 1 < a.tiles) gside.unit_entry(a.side1, (tile + 1) * groups, bits, b1);
-      e0 = b0;
-      e1 = tile + 1 < a.tiles ? b1 : a.n_exc;
-    }
-    // Golay70's list holds 14-byte records: the window of record e is 16 bytes
-    // from (14·e) & ~3, so the tile's windows end by 14·e1 + 2, which rounded
-    // up to 16 stays inside side0's 16 bytes of padding; Planes12x's entries
-    // are 16 bytes, aligned
-    side.exc_start = (e0 * kExcEntry) & ~15ull;
-    const uint64_t end = e1 * kExcEntry + (kExcEntry == kPlanes14Bytes ? 2 : 0);
-    exc_chunks = (end - side.exc_start + 15) / 16;
-    side.exc_in_lds = kExcLds && exc_chunks * 16 <= (uint64_t)kExcLdsBytes;
+    const uint64_t e0 = ((const uint32_t*)a.side1)[tile];
+    const uint64_t e1 = tile + 1 < a.tiles ? ((const uint32_t*)a.side1)[tile + 1] : a.n_exc;
+    side.excbase = (uint32_t)e0;
     exc_first = (uint32_t)e0;
     exc_count = (uint32_t)(e1 - e0);
   }
@@ -969,7 +902,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // then the pipeline's record loads, then the LDS writes, which wait only for
   // the older staging loads.
   constexpr int kXPer = XPER;                  // x blocks per thread held in registers
-  constexpr int kEPer = kExcLdsBytes / 16 / (kMaxWaves * 64), kUPer = 2;
+  constexpr int kEPer = kExcPrefetch, kUPer = 2;
   // rare overflow first (xblocks > kXPer·threads, or fewer threads than
   // classes): loads of unknown count here, before the ordered ones.  Only the
   // ball's class ids occur in a layout, so only their entries are staged, both
@@ -1015,16 +948,12 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         t2[c] = make_entry_as<LAYOUT>(a.table, (uint32_t)c, cen0b, cen1b);
         t2[c + 512] = make_entry_as<LAYOUT>(a.table, (uint32_t)c | 512u, cen0b, cen1b);
       }
-      if constexpr (LAYOUT == LEECH_GOLAY70) gs[c] = make_g70(a.table, (uint32_t)c);
+      if constexpr (LAYOUT == LEECH_GOLAY70) p14t[c] = *(const u32x2a*)&a.table[c];
     }
   const uint8_t* side_units = LAYOUT == LEECH_SLOT32 ? a.side0 : a.side1;
   if constexpr (kUnits)
     for (int u = tid + kUPer * nthr; u < groups; u += nthr)
       ((u32x4a*)units_lds)[u] = ((const u32x4a*)side_units)[tile * groups + u];
-  if constexpr (kExcLds)
-    if (side.exc_in_lds)
-      for (int64_t c = tid + (int64_t)kEPer * nthr; c < (int64_t)exc_chunks; c += nthr)
-        ((u32x4a*)exc_lds)[c] = ((const u32x4a*)(a.side0 + side.exc_start))[c];
   // x and the class table through buffer descriptors: a wave with no block
   // (no class) to stage loads through the null descriptor, and lanes past nb
   // read zeros, which is the padding past the last column
@@ -1088,10 +1017,10 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   }
   if constexpr (kExc) {
-    // Planes12x: the tile's exception entries, for the hoisted decoder
-    const uint64_t n_chunks =
-        (kExcLds ? side.exc_in_lds : !a.inline_exc) ? exc_chunks : 0;
-    const __amdgpu_buffer_rsrc_t re = make_rsrc(a.side0 + side.exc_start, n_chunks * 16);
+    // the tile's exception entries, for the hoisted decoder
+    const uint64_t n_chunks = !a.inline_exc ? exc_count : 0;
+    const __amdgpu_buffer_rsrc_t re =
+        make_rsrc(a.side0 + (uint64_t)exc_first * kExcEntryBytes, n_chunks * kExcEntryBytes);
 #pragma unroll
     for (int q = 0; q < kEPer; ++q) {
       const __amdgpu_buffer_rsrc_t r = (uint64_t)(q * nthr + wave * 64) < n_chunks ? re : null_rsrc();
@@ -1125,6 +1054,11 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       e.thi = tr.y;
       e.aux = tr.w & 0xFFu;
       if constexpr (LAYOUT == LEECH_PLANES12X) e = p12_entry(tr.x, tr.y, 0.0f);
+      if constexpr (LAYOUT == LEECH_GOLAY70) {
+        g70_table(tr2, e.tlo, e.thi);
+        e.aux = 0u;
+        p14t[tid] = u32x2a{tr.x, tr.y};
+      }
       const float f = __builtin_bit_cast(float, (uint32_t)tr.z) * kTwo24;
       e.factor = f * cen0;
       ts[tid] = e;
@@ -1137,7 +1071,6 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         e.factor = f * cen1b;
         t2[tid + 512] = e;
       }
-      if constexpr (LAYOUT == LEECH_GOLAY70) gs[tid] = g70_entry(tr, tr2);
     }
     if constexpr (LAYOUT == LEECH_GOLAY70)
       if (tid < 32) ((u32x4a*)cws)[tid] = gr;
@@ -1146,13 +1079,6 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
 #pragma unroll
     for (int q = 0; q < kUPer; ++q)
       if (tid + q * nthr < groups) ((u32x4a*)units_lds)[tid + q * nthr] = ur[q];
-  }
-  if constexpr (kExcLds) {
-    if (side.exc_in_lds) {
-#pragma unroll
-      for (int q = 0; q < kEPer; ++q)
-        if (tid + q * nthr < (int64_t)exc_chunks) ((u32x4a*)exc_lds)[tid + q * nthr] = er[q];
-    }
   }
   __syncthreads();
 #pragma unroll
@@ -1166,34 +1092,39 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   };
   auto tab = [&](uint32_t e16) -> LdsEntry {
     // a power-of-two copy size lets the offset be or'ed into the field's mask
-    return tab_at(LAYOUT == LEECH_PLANES12X ? e16 + toff : e16 | toff);
+    return tab_at(kExc ? e16 + toff : e16 | toff);
   };
-  auto tab14 = [&](uint32_t e16) -> LdsEntry {
-    if constexpr (LAYOUT == LEECH_PLANES12X) return p12_as14(tab(e16));
-    else return tab(e16);
+  // the entry of a decoded field in the table copy at byte offset off, as a
+  // Planes14 table
+  auto as14 = [&](uint32_t e16, uint32_t off) -> LdsEntry {
+    LdsEntry t = tab_at(kExc ? e16 + off : e16 | off);
+    if constexpr (LAYOUT == LEECH_PLANES12X) t = p12_as14(t);
+    if constexpr (LAYOUT == LEECH_GOLAY70) {
+      const u32x2a pt = p14t[(e16 >> 4) & 511u];
+      t.tlo = pt.x;
+      t.thi = pt.y;
+    }
+    return t;
   };
-  auto g70 = [&](uint32_t c) -> G70Entry { return gs[c]; };
+  auto tab14 = [&](uint32_t e16) -> LdsEntry { return as14(e16, toff); };
   auto cw = [&](uint32_t m) -> uint32_t { return golay_word(cws, m); };
 
-  // Hoisted exception decoder (Planes12x, Golay70): the tile's exceptions
-  // (their exact Planes14 records are in LDS) are decoded once, densely,
-  // before the loop, and each one's contribution dot12 · factor is kept in
-  // LDS; the loop then runs the layout's own decode alone and a lane holding
-  // an exception takes the kept value in place of its own.  Same products,
-  // same order: y is unchanged.
+  // Hoisted exception decoder (Planes12x, Golay70): each of the tile's
+  // exceptions is decoded once, densely, before the loop, into a table entry
+  // of its own at the entry number its record holds (in its row's table
+  // copy): no table bytes, so the loop's lookups give zeros and its sum is +0,
+  // and the exception's contribution dot12 · factor as the added term, so the
+  // loop's fma(sum, factor, added) yields that contribution exactly.  Same
+  // products, same order as decoding the exact record in the loop: y is
+  // unchanged, and the loop has no branch, select or count for exceptions.
   bool hoisted = false;
-  if constexpr (LAYOUT == LEECH_PLANES12X) {
-    // Planes12x: each exception gets a table entry of its own, at the entry
-    // number its record holds (in its row's table copy): no magnitudes, so the
-    // loop's lookups give zeros and its sum is +0, and the exception's
-    // contribution dot12 · factor as the added term, so the loop's
-    // fma(sum, factor, added) gives that contribution exactly.
+  if constexpr (kExc) {
     hoisted = !a.inline_exc;
     if (hoisted) {
       auto keep = [&](uint32_t e, const u32x4a& w) {
         // the entry names the block's slot in the tile; units are R_t × C
         // blocks in column order
-        const uint32_t slot = w.w >> (kP12PosShift - 96);
+        const uint32_t slot = w.w >> (kExcSlotShift - 96);
         const int unit = min((int)(slot / (uint32_t)(R_t * C)), gf);
         const uint32_t ul = slot - (uint32_t)(unit * R_t * C);
         const uint32_t cols = unit == gf ? (uint32_t)C_last : (uint32_t)C;
@@ -1204,62 +1135,20 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
         uint32_t e16, W[3], h[12];
         p14_record(w.x, w.y, w.z, w.w, 0u, 28u, W, e16);
         const uint32_t off = two && (int)(ul / cols) >= split ? a.tab_bytes : 0u;
-        const LdsEntry te = p12_as14(tab_at(e16 + off));
+        const LdsEntry te = as14(e16, off);
         p14_core(W, te.tlo, te.thi, h);
         LdsEntry k;
         k.tlo = 0u;
         k.thi = 0u;
         k.factor = 0.0f;
         k.aux = __builtin_bit_cast(uint32_t, dot12(h, xw) * te.factor);
-        *(LdsEntry*)(smem + ((kP12ExcEntry0 + e) << 4) + off) = k;
+        *(LdsEntry*)(smem + ((kExcEntry0 + e) << 4) + off) = k;
       };
 #pragma unroll
       for (int q = 0; q < kEPer; ++q)
         if (tid + q * nthr < (int)exc_count) keep(tid + q * nthr, er[q]);
       for (uint32_t e = tid + kEPer * nthr; e < exc_count; e += nthr)
-        keep(e, *(const u32x4a*)(a.side0 + (uint64_t)(exc_first + e) * kP12EntryBytes));
-      __syncthreads();
-    }
-  } else if constexpr (kExc) {
-    hoisted = !a.inline_exc && side.exc_in_lds;
-    if (hoisted) {
-      for (uint32_t e = tid; e < exc_count; e += nthr) {
-        const uint32_t ex = exc_first + e;
-        uint32_t w[4], sh;
-        side.template exc_window<kExcEntry>(ex, w, sh);
-        int unit;
-        uint32_t ul;
-        {
-          // its unit: the last one whose first exception index is ≤ ex
-          int lo = 0, hi = groups - 1;
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            uint64_t b;
-            uint32_t base;
-            side.unit_entry(nullptr, tile * groups + mid, b, base);
-            if (base <= ex) lo = mid;
-            else hi = mid - 1;
-          }
-          uint64_t bits;
-          uint32_t base;
-          side.unit_entry(nullptr, tile * groups + lo, bits, base);
-          for (uint32_t k = ex - base; k; --k) bits &= bits - 1;   // its place in the unit
-          unit = lo;
-          ul = (uint32_t)__builtin_ctzll(bits);
-        }
-        const uint32_t cols = unit == gf ? (uint32_t)C_last : (uint32_t)C;
-        const uint32_t* xj = xs + 12 * (unit * C + ul % cols);
-        uint32_t xw[12];
-#pragma unroll
-        for (int k = 0; k < 12; ++k) xw[k] = xj[k];
-        uint32_t e16, W[3], h[12];
-        p14_record(w[0], w[1], w[2], w[3], sh, (sh + 28u) & 31u, W, e16);
-        // the table of the block's own row (ul / cols of its tile)
-        const LdsEntry te = tab_at(e16 | (two && (int)(ul / cols) >= split ? a.tab_bytes : 0u));
-        p14_core(W, te.tlo, te.thi, h);
-        pre[e] = dot12(h, xw) * te.factor;
-      }
-      if (tid == 0) pre[exc_count] = 0.0f;
+        keep(e, gside.exc_entry((uint64_t)exc_first + e));
       __syncthreads();
     }
   }
@@ -1282,42 +1171,29 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       acc[0] += dot12(ones, xw);
     } else {
       uint32_t h[12], e16;
-      if constexpr (LAYOUT == LEECH_PLANES12X) {
+      if constexpr (kExc) {
         if (hoisted) {
           // the record's entry field addresses the class's entry or the
           // exception's own (added term = its kept contribution)
-          const LdsEntry te = tab_at(lshl4_add(pr.w0 & 0xFFFu, toff));
-          p12_core(pr.w0, pr.w1, pr.w2, te.thi, h);
+          LdsEntry te;
+          if constexpr (LAYOUT == LEECH_PLANES12X) {
+            te = tab_at(lshl4_add(pr.w0 & 0xFFFu, toff));
+            p12_core(pr.w0, pr.w1, pr.w2, te.thi, h);
+          } else {
+            const uint32_t r0 = align(pr.w1, pr.w0, pr.sh), r1 = align(pr.w2, pr.w1, pr.sh);
+            const uint32_t r2 = pr.w2 >> pr.sh;
+            te = tab_at(lshl4_add(r0 & 0xFFFu, toff));
+            golay70_core(align(r1, r0, kG70C0Pos), align(r2, r1, kG70C1Pos - 32),
+                         cw(r0 >> kG70MsgPos & 0xFFFu), te.tlo, te.thi, h);
+          }
           float v = __builtin_fmaf(dot12(h, xw), te.factor, __builtin_bit_cast(float, te.aux));
           if constexpr (decltype(last)::value) v = L.own ? v : 0.0f;
           acc[0] = __builtin_fmaf((float)as_half(pr.scale), v, acc[0]);
           return;
         }
       }
-      if constexpr (LAYOUT == LEECH_GOLAY70) {
-        if (hoisted) {
-          const uint32_t r0 = align(pr.w1, pr.w0, pr.sh), r1 = align(pr.w2, pr.w1, pr.sh);
-          const uint32_t r2 = pr.w2 >> pr.sh;
-          e16 = (r0 << 4) & 0x3FF0u;
-          golay70_core(align(r1, r0, 22), align(r2, r1, 14), cw((r0 >> 10) & 0xFFFu),
-                       g70((e16 >> 4) & 511u), h);
-          float v = dot12(h, xw) * tab(e16).factor;
-          uint64_t bits;
-          uint32_t base;
-          side.unit_entry(nullptr, tile * groups + g, bits, base);
-          const uint32_t ei =
-              base - exc_first + (uint32_t)__builtin_popcountll(bits & ((1ull << L.ul) - 1ull));
-          // a stand-in lane (past the last column) has zero x and must add
-          // zero, not the contribution kept for the block it stands in for
-          const float kept = pre[min(ei, exc_count)];
-          v = ((r2 >> 6) & 1u) && L.own ? kept : v;
-          acc[0] = __builtin_fmaf((float)as_half(pr.scale), v, acc[0]);
-          return;
-        }
-      }
       LdsEntry te;
-      decode_block<LAYOUT>(pr, L.ul, tile, tile * groups + g, tab, tab14, g70, cw, side, a, h,
-                           e16, te);
+      decode_block<LAYOUT>(pr, tile, tab, tab14, cw, side, h, e16, te);
       const float sc = (float)as_half(pr.scale), f = te.factor;
       acc[0] = __builtin_fmaf(sc, dot12(h, xw) * f, acc[0]);
 #pragma unroll
@@ -1430,12 +1306,10 @@ __global__ __launch_bounds__(256) void decode_kernel(GemvArgs a, int8_t* zout, u
     return make_entry_as<LAYOUT>(a.table, e16 >> 4, 1.0f, 1.0f);
   };
   auto tab14 = [&](uint32_t e16) -> LdsEntry { return make_entry(a.table, e16 >> 4, 1.0f, 1.0f); };
-  auto g70 = [&](uint32_t c) -> G70Entry { return make_g70(a.table, c); };
   auto cw = [&](uint32_t m) -> uint32_t { return golay_word(a.codewords, m); };
   uint32_t h[12], e16;
   LdsEntry te;
-  decode_block<LAYOUT>(p, ul, tile, tile * (int)a.groups + g, tab, tab14, g70, cw, side, a, h,
-                       e16, te);
+  decode_block<LAYOUT>(p, tile, tab, tab14, cw, side, h, e16, te);
   int8_t z[kDim];
 #pragma unroll
   for (int k = 0; k < 12; ++k) {
@@ -1549,7 +1423,7 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
   const size_t table = LAYOUT == kNoWeights ? 0 : (a.tab2 ? 2 : 1) * (size_t)a.tab_bytes;
   return table + (size_t)NB * a.groups * a.C * 48 + (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
-         (LAYOUT == LEECH_GOLAY70 ? kExcLdsBytes + kPreFloats * 4 : 0) + red;
+         red;
 }
 
 template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0>
@@ -1604,12 +1478,12 @@ static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
 template <int LAYOUT, int NB = 1>
 static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
   GemvArgs a = a0;
-  if constexpr (LAYOUT == LEECH_PLANES12X) {
+  if constexpr (has_exc<LAYOUT>()) {
     // the hoisted decoder keeps the tile's exceptions as table entries after
     // the 1024 class entries; where they do not fit in LDS, exceptions are
     // decoded in the loop
     if (!a.inline_exc) {
-      a.tab_bytes = (uint32_t)(kP12ExcEntry0 + a.tile_exc_max) * (uint32_t)sizeof(LdsEntry);
+      a.tab_bytes = (uint32_t)(kExcEntry0 + a.tile_exc_max) * (uint32_t)sizeof(LdsEntry);
       if (gemv_lds_bytes<LAYOUT, NB>(a) > 160 * 1024) {
         a.inline_exc = 1;
         a.tab_bytes = kTableBytes;

@@ -79,7 +79,7 @@ constexpr int kUnitEntryBytes = 16;  // per-unit side entry: u64 bitmap, u32 bas
 
 // Planes12x record (96 bits, little-endian from its first byte, words W0, W1,
 // W2): bits [0, 12) hold the block's table entry, class | gain << 9, or, for a
-// block with five levels, kP12ExcEntry0 + its index in its tile's exception
+// block with five levels, kExcEntry0 + its index in its tile's exception
 // list; the other 84 bits hold the 12 pairs of coordinates in the GEMV's
 // consumption order, each as one selector word taken straight from the
 // record.  Pair q's selector word is (kP12Sel[q]): word w rotated right by s
@@ -88,9 +88,7 @@ constexpr int kUnitEntryBytes = 16;  // per-unit side entry: u64 bitmap, u32 bas
 // 8 + k that coordinate's non-negative bit, bits 16, 17 and 24 + l the same
 // of kPairCoords[q][1].  Bits of the record no selector names are zero.  A
 // five-level block carries only its entry field; its exact Planes14 record is
-// in the exception list.  An exception entry is 16 bytes: the block's exact
-// Planes14 record (14 bytes, bits [106, 112) zero) with the block's storage
-// slot inside its tile in bits [106, 128).
+// in the exception list.
 struct P12Sel {
   int rot, word, shift, k, l;
 };
@@ -122,11 +120,21 @@ __host__ __device__ constexpr bool p12_layout_ok() {
   return true;
 }
 static_assert(p12_layout_ok(), "Planes12x pair selectors overlap");
-constexpr int kP12EntryBytes = 16;
-constexpr int kP12PosShift = 106;
-constexpr int kP12PosBits = 22;
-constexpr uint32_t kP12ExcEntry0 = 1024;        // entry of a tile's first exception
-constexpr uint32_t kP12ExcMax = 4096 - 1024;    // exceptions one tile may hold
+// Exceptions of Planes12x and Golay70: a block whose record cannot hold it
+// carries only its table entry field, kExcEntry0 + its index in its tile's
+// exception list; a list entry is 16 bytes, the block's exact Planes14 record
+// (14 bytes, bits [106, 112) zero) with the block's storage slot inside its
+// tile in bits [106, 128); lists follow each other in tile order and a u32 per
+// tile gives the index of its first entry.
+constexpr int kExcEntryBytes = 16;
+constexpr int kExcSlotShift = 106;
+constexpr int kExcSlotBits = 22;
+constexpr uint32_t kExcEntry0 = 1024;        // entry of a tile's first exception
+constexpr uint32_t kExcMax = 4096 - 1024;    // exceptions one tile may hold
+// Golay70 record (72 bits): table entry field [0, 12) (class | gain << 9, or
+// an exception's), codeword message [12, 24), low code plane [24, 48), high
+// code plane [48, 72) (bit i of each = coordinate i).
+constexpr int kG70MsgPos = 12, kG70C0Pos = 24, kG70C1Pos = 48;
 
 // Device class record: 32 bytes per class id (LEECH_DEVICE_TABLE_BYTES / 512).
 //   perm[8]   : byte table read by v_perm_b32: perm[0] = 0x80 (the binary16

@@ -1,7 +1,9 @@
-"""The two exception decoders of Planes12x and Golay70 (hoisted pre-pass, in
-line) through the C ABI: bit-identical y to each other and to Planes14, and to
-the oracle within tolerance, on the usual shapes and on a tile whose exception
-records exceed the LDS budget (decoded from global memory in both modes)."""
+"""The two exception decoders of Planes12x and Golay70 (hoisted: each exception
+kept as a table entry of its own; in line: decoded in the loop) through the C
+ABI: bit-identical y to each other and to Planes14, and to the oracle within
+tolerance, on the usual shapes, on a tile made only of exceptions, and on a
+grouped launch whose two table copies with 3072 exception entries each exceed
+the LDS budget (decoded in line whichever mode is asked for)."""
 import sys
 
 import numpy as np
@@ -47,6 +49,7 @@ def check(dev, dcb, inp, label, layout):
     cls, sm, lv = dcb.cb.fields_from_points(inp.z)
     g70 = P.LeechMatrix.from_fields(dcb, layout, cls, inp.gain, sm, lv, inp.scale, dev)
     p14 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    assert (p14.desc.lane_cols, p14.desc.tile_rows) == (g70.desc.lane_cols, g70.desc.tile_rows)
     say(f"[exception modes] {P.LAYOUT_NAMES[layout]} {label}: {g70.desc.n_exceptions} "
         f"exceptions of {inp.M * inp.nb}")
     x = torch.from_numpy(inp.x).to(dev)
@@ -74,8 +77,9 @@ def test_modes_agree(dev, dcb, M, K, layout):
 def exception_points(cb, layout, n, seed):
     """n drawn points that are exceptions of the layout.  Planes12x: points of
     five-level classes.  Golay70: points its 2-bit code cannot hold, which the
-    host expansion of a one-column matrix flags (record bit 70; with one block
-    per row the storage slot of row r is r)."""
+    host expansion of a one-column matrix flags (an exception record's entry
+    field, bits [0, 12), is 1024 or more; with one block per row the storage
+    slot of row r is r)."""
     pool = synth.sample_ball_points(synth.rng_for(seed, "exc-pool"), 40 * n)
     cls, sm, lv = cb.fields_from_points(pool)
     if layout == P.PLANES12X:
@@ -84,18 +88,18 @@ def exception_points(cb, layout, n, seed):
         gain = np.zeros(len(pool), np.uint8)
         d, main, _, _ = P.expand_layout(cb, P.GOLAY70, cls[:, None], gain[:, None], sm[:, None],
                                         lv[:, None, :])
-        flags = ((main[: 9 * len(pool)].reshape(-1, 9)[:, 8] >> 6) & 1) == 1
+        rec = main[: 9 * len(pool)].reshape(-1, 9).astype(np.uint32)
+        flags = ((rec[:, 0] | rec[:, 1] << 8) & 0xFFF) >= 1024
     picked = pool[flags]
     assert len(picked) >= n, "pool too small"
     return picked[:n]
 
 
 @pytest.mark.parametrize("layout", EXC_LAYOUTS, ids=["planes12x", "golay70"])
-def test_tile_over_the_lds_budget(dev, dcb, layout):
-    """8 × 14400: lane_cols 16, two tiles of 4 rows × 600 blocks.  The first
-    tile holds only exceptions (2400 records, more than the 32 KiB staged in
-    LDS): it is decoded in line from global memory in both modes; the second
-    is an ordinary tile."""
+def test_tile_of_exceptions(dev, dcb, layout):
+    """8 × 14400: geometry 16 × 4, two tiles of 4 rows × 600 blocks.  The first
+    tile holds only exceptions (2400 entries after the table's 1024 class
+    entries); the second is an ordinary tile."""
     M, K = 8, 14400
     inp = synth.make_gemv_inputs(M, K, seed=31, name="exc-heavy")
     z = inp.z.copy()
@@ -111,3 +115,42 @@ def test_tile_over_the_lds_budget(dev, dcb, layout):
 def test_mode_is_validated():
     with pytest.raises(P.LeechError, match="LEECH_E_ARG"):
         P.set_exception_mode(7)
+
+
+@pytest.mark.parametrize("layout", EXC_LAYOUTS, ids=["planes12x", "golay70"])
+def test_exceptions_over_the_lds_budget(dev, dcb, layout):
+    """8 × 18432 (768 blocks a row), geometry 16 × 4, the first tile all
+    exceptions (3072, the most a tile may hold), launched as two row groups
+    [2, 6] so that tile 0 holds rows of both groups: two table copies of
+    (1024 + 3072) entries (128 KiB) and the activation exceed the 160 KiB of
+    LDS, so the exceptions are decoded in line in either mode.  Every row
+    matches the oracle with its own group's centroids, and both modes and
+    Planes14 give the same bits."""
+    M, K = 8, 18432
+    inp = synth.make_gemv_inputs(M, K, seed=33, name="exc-budget")
+    z = inp.z.copy()
+    z[:4] = exception_points(dcb.cb, layout, 4 * inp.nb, seed=33).reshape(4, inp.nb, 24)
+    cls, sm, lv = dcb.cb.fields_from_points(z)
+    mat = P.LeechMatrix.from_fields(dcb, layout, cls, inp.gain, sm, lv, inp.scale, dev)
+    p14 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    assert mat.desc.tile_exc_max == 3072 and mat.desc.tile_rows == 4
+    say(f"[exception modes] {P.LAYOUT_NAMES[layout]} over the budget: "
+        f"{mat.desc.n_exceptions} exceptions")
+    x = torch.from_numpy(inp.x).to(dev)
+    rows, cens = [2, 6], [(0.75, 1.25), (1.1, 0.9)]
+    ys = []
+    for mode in (P.EXC_HOISTED, P.EXC_INLINE):
+        P.set_exception_mode(mode)
+        try:
+            ys.append(mat.gemv_grouped(x, rows, cens).cpu().numpy())
+        finally:
+            P.set_exception_mode(P.EXC_HOISTED)
+    yp = p14.gemv_grouped(x, rows, cens).cpu().numpy()
+    assert np.array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
+    assert np.array_equal(ys[0].view(np.uint32), yp.view(np.uint32))
+    r0 = 0
+    for n, c in zip(rows, cens):
+        W = D.weights64_from_points(z[r0:r0 + n], inp.gain[r0:r0 + n], inp.scale[r0:r0 + n], c)
+        e = D.errors(ys[0][r0:r0 + n], D.gemv64(W, inp.x), W, inp.x)
+        assert e["max_norm_err"] <= 2e-3 and e["max_abs_err"] <= 1e-5, e
+        r0 += n

@@ -120,7 +120,9 @@ def test_record_sizes_and_exceptions(cb):
     ds = P.expand_layout(cb, P.SLOT32, cls, inp.gain, sm, lv)[0]
     assert ds.main_bytes == 16 * n + 4 * five + 16
     dg = P.expand_layout(cb, P.GOLAY70, cls, inp.gain, sm, lv)[0]
-    assert dg.main_bytes == 9 * n + 16 and dg.side_bytes[0] == 14 * dg.n_exceptions + 16
+    assert dg.main_bytes == 9 * n + 16 and dg.side_bytes[0] == 16 * dg.n_exceptions + 16
+    assert dg.side_bytes[1] == 4 * -(-256 // dg.tile_rows)
+    assert d12.tile_exc_max >= -(-five // -(-256 // d12.tile_rows)) and dg.tile_exc_max > 0
     assert 0 < dg.n_exceptions < 0.08 * n
 
 
