@@ -23,9 +23,9 @@ the same GEMV timed over one whole ≥ 1 GiB cycle of replicas beside it.
 Printed: one JSON line with the metric (served-weight GB/s of the Planes14
 GEMV), µs per GEMV, the roofline against MI355X's 8 TB/s, every arm of the
 layout comparison (four layouts, FP16 GEMV control, no-weights control;
-interleaved, 7 rounds, first 2 discarded, medians), the decoder-layer,
-batch, large-matrix and launch-floor sections, and the CPU oracle timed on a
-bounded sample of the same workload.
+interleaved, 7 rounds, first 2 discarded, medians), the prologue-mode and
+phase breakdowns, the decoder-layer, batch, large-matrix and launch-floor
+sections, and the CPU oracle timed on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -361,6 +361,58 @@ def prologue_table(args, torch, P, arm):
             res[m].append(timed_replay(torch, ev, g) * 1e3 / k)
     del graphs
     return {str(m): round(statistics.median(v), 3) for m, v in res.items()}
+
+
+def phase_table(torch, P, arm, x, y, steps=20):
+    """Where a launch's time goes: `steps` back-to-back Planes14 launches over
+    the arm's replicas (as the timed region: a graph behind the eviction
+    replay), each recording per-workgroup stamps of the 100 MHz real-time
+    counter (leech_gemv_phases: start, staging barrier passed, each wave's last
+    unit decoded, last store).  Medians over launches of: the gap between one
+    launch's last store and the next one's first workgroup start; the spread
+    of workgroup starts; and, per workgroup (median over workgroups), the
+    prologue (start to barrier), the loop (barrier to the last wave's last
+    unit) and the tail (to the last store); the event-timed µs per launch and
+    the counter rate it implies beside them."""
+    import numpy as np
+    mats = arm.mats
+    n = len(mats)
+    d = mats[0].desc
+    tiles = -(-d.M // d.tile_rows)
+    waves = min(8, -(-d.nb // d.lane_cols))
+    st = torch.full((steps, tiles, 11), -1, dtype=torch.int64, device=x.device)
+    g = torch.cuda.CUDAGraph()
+    mats[0].gemv_phases(x, y, st[0])
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            mats[i % n].gemv_phases(x, y, st[i])
+    start, length, _ = arm.evict_plan(steps)
+    lead = arm.graph(torch, length, start)
+    g.replay()
+    ms = timed_replay(torch, lead, g)
+    s = st.cpu().numpy().astype(np.float64)
+    del g
+    t0, t1, t10 = s[:, :, 0], s[:, :, 1], s[:, :, 10]
+    tw = s[:, :, 2:2 + waves].max(axis=2)
+    starts, ends = t0.min(axis=1), t10.max(axis=1)
+    span_ticks = ends[-1] - starts[0]
+    mhz = span_ticks / (ms * 1e3) if ms > 0 else float("nan")
+    # ticks to µs at the rate that makes the stamped span of the replay equal
+    # its event-timed span (the counter is nominally 100 MHz)
+    us = lambda v: round(float(v) / mhz, 3)  # noqa: E731
+    med = lambda v: us(np.median(v))  # noqa: E731
+    return {"launches": steps, "workgroups": tiles, "waves": waves,
+            "event_us_per_launch": round(ms * 1e3 / steps, 3),
+            "counter_MHz_implied": round(float(mhz), 2),
+            "gap_between_launches_us": med(starts[1:] - ends[:-1]),
+            "workgroup_start_spread_us": med(t0.max(axis=1) - starts),
+            "prologue_us": med(np.median(t1 - t0, axis=1)),
+            "loop_us": med(np.median(tw - t1, axis=1)),
+            "tail_us": med(np.median(t10 - tw, axis=1)),
+            "first_start_to_last_store_us": med(ends - starts),
+            "span_us_by_launch": [us(v) for v in ends - starts],
+            "gap_us_by_launch": [us(v) for v in starts[1:] - ends[:-1]]}
 
 
 def shader_clock(torch, arm, seconds=1.0):
@@ -1241,6 +1293,9 @@ def main():
 
     prologue = {f"{inp.M}x{inp.K}": prologue_table(args, torch, P, main_arm)}
     log(f"[bench] prologue modes {prologue}")
+    x_main = torch.from_numpy(inp.x).to(main_arm.mats[0].main.device)
+    phases = {f"{inp.M}x{inp.K}": phase_table(torch, P, main_arm, x_main, y_arms)}
+    log(f"[bench] phases {phases}")
 
     # layout comparison: arms interleaved in fixed order, rounds, first discarded
     table = arms_table(args, torch, arms, inp)
@@ -1259,6 +1314,9 @@ def main():
                     "arms": arms_table(args, torch, arms4, inp4)}
         prologue[f"{inp4.M}x{inp4.K}"] = prologue_table(args, torch, P, arms4["planes14"])
         log(f"[bench] prologue modes {prologue}")
+        x4 = torch.from_numpy(inp4.x).to(y4.device)
+        phases[f"{inp4.M}x{inp4.K}"] = phase_table(torch, P, arms4["planes14"], x4, y4)
+        log(f"[bench] phases {phases}")
         del arms4, y4
         torch.cuda.empty_cache()
 
@@ -1339,6 +1397,7 @@ def main():
         "arms": table,
         "arms_c4": table_c4,
         "prologue_modes_us": prologue,
+        "phases": phases,
         "verified": verified,
         "batch": batch,
         "layer_8b": layer,

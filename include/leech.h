@@ -357,6 +357,21 @@ int leech_set_exception_mode(int mode);
 enum { LEECH_PROLOGUE_AUTO = -1 };
 int leech_set_prologue_mode(int mode);
 
+/* Measurement launch: leech_gemv (PLANES14 only; LEECH_E_LAYOUT otherwise)
+ * that also records, per workgroup t, 11 u64 stamps of the GPU's 100 MHz
+ * real-time counter at d_stamps[11·t + k] (caller-owned device memory, 8-byte
+ * aligned, 11 · ceil(M / tile_rows) entries): k = 0 the first wave's start,
+ * 1 the first wave past the staging barrier (x and the class table in LDS),
+ * 2 + w wave w's last unit decoded (w < the launch's waves; the rest are not
+ * written), 10 the first wave's last y store issued.  The work and y are
+ * leech_gemv's; the stamps cost one counter read and one store each.  For the
+ * phase breakdown of a launch (§3.4 attributes the gap to the DRAM floor to
+ * latency, occupancy and staging). */
+int leech_gemv_phases(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                      const void* d_side1, const void* d_class_table, const void* d_codewords,
+                      const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
+                      float* d_y, uint64_t* d_stamps, void* stream);
+
 /* GEMV behind the activation rotation in one launch (§2.3: the activation is
  * rotated before the matvec; §6: every consumer rotates): y = W · R(x), where
  * R is leech_rotate_x's blockwise Walsh–Hadamard rotation of the raw binary16

@@ -122,6 +122,24 @@ class LeechMatrix:
                   self.scale.data_ptr(), centroids, x.data_ptr(), y.data_ptr(), _stream(stream))
         return y
 
+    def gemv_phases(self, x, y, stamps, centroids=(1.0, 1.0), stream=None):
+        """gemv with per-workgroup phase stamps (leech_gemv_phases): stamps is a
+        contiguous int64 device tensor of at least 11 · tiles entries."""
+        torch = _torch()
+        tiles = -(-self.M // self.desc.tile_rows)
+        if (stamps.dtype != torch.int64 or not stamps.is_contiguous()
+                or stamps.numel() < _lib.PHASE_STAMPS * tiles):
+            raise ValueError("stamps must be a contiguous int64 tensor of 11 * tiles entries")
+        if x.dtype != torch.float16 or x.numel() != self.Kpad or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 tensor of length Kpad")
+        if y.dtype != torch.float32 or y.numel() != self.M or not y.is_contiguous():
+            raise ValueError("y must be a contiguous f32 tensor of length M")
+        m, s0, s1 = self._ptrs()
+        _lib.gemv_phases(self.desc, m, s0, s1, self.dcb.table.data_ptr(),
+                         self.dcb.golay_gen.data_ptr(), self.scale.data_ptr(), centroids,
+                         x.data_ptr(), y.data_ptr(), stamps.data_ptr(), _stream(stream))
+        return y
+
     def gemv_batch(self, X, Y=None, centroids=(1.0, 1.0), stream=None):
         """Y[b] = W X[b]: X fp16 [B, Kpad] device tensor (row stride a multiple
         of 8), Y f32 [B, M]; each block decoded once for up to 8 activations."""

@@ -30,7 +30,7 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
            "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch",
            "leech_gemv_rotated", "leech_set_prologue_mode", "leech_expand_layout_tiled",
-           "leech_layout_geometry"]
+           "leech_layout_geometry", "leech_gemv_phases"]
 
 
 class LeechError(RuntimeError):
@@ -84,6 +84,7 @@ def _load() -> C.CDLL:
         "leech_layout_scales": (I, [C.POINTER(LayoutDesc), P, P]),
         "leech_host_decode_layout": (I, [P, C.POINTER(LayoutDesc), P, P, P, P, P, P]),
         "leech_gemv": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P, P]),
+        "leech_gemv_phases": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P, P, P]),
         "leech_gemv_grouped": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, I, P, P, P, P, P]),
         "leech_decode_blocks": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, P, P]),
         "leech_fp16_gemv_ref": (I, [I64, I64, P, P, P, P]),
@@ -267,6 +268,17 @@ def gemv(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroid
     check(lib.leech_gemv(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
                          d_codewords or None, d_scale, C.cast(cen, C.c_void_p), d_x, d_y,
                          stream or None))
+
+
+PHASE_STAMPS = 11
+
+
+def gemv_phases(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroids, d_x,
+                d_y, d_stamps, stream=0):
+    cen = (C.c_float * 2)(float(centroids[0]), float(centroids[1]))
+    check(lib.leech_gemv_phases(C.byref(desc), d_main, d_side0 or None, d_side1 or None, d_table,
+                                d_codewords or None, d_scale, C.cast(cen, C.c_void_p), d_x, d_y,
+                                d_stamps, stream or None))
 
 
 def gemv_batch(desc, d_main, d_side0, d_side1, d_table, d_codewords, d_scale, centroids, batch,

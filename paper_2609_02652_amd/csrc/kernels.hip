@@ -126,7 +126,14 @@ struct GemvArgs {
   int64_t K;
   int rot_k;
   float rot_norm;
+  // phase stamps (measurement launches): kPhaseStamps u64 per workgroup
+  uint64_t* stamps;
 };
+// Phase stamps of a measurement launch, per workgroup, in the 100 MHz
+// real-time counter: 0 the first wave's start, 1 the first wave past the
+// staging barrier, 2 + w wave w's last unit decoded, 10 the first wave's
+// last y store issued.
+constexpr int kPhaseStamps = 11;
 
 // Where side data comes from: global memory (verification decode, and the
 // GEMV prologue before LDS is written), or the tile's copy in LDS.  Slot32
@@ -830,7 +837,11 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // (Planes14, NB = 1): blockwise Walsh–Hadamard with the caller's signs, the
 // stages in the order and arithmetic of leech_rotate_x, so the staged binary16
 // activation is bit-identical to that call's output.
-template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false, int PRO = 0>
+// PHASE: a measurement launch that records kPhaseStamps real-time stamps per
+// workgroup (lane 0 of the stamping wave, a vector store each); the work is
+// the plain launch's.
+template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false, int PRO = 0,
+          bool PHASE = false>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   constexpr int kPrefetch = pro_prefetch(PRO);        // units in flight per wave
   constexpr int kFirstUnits = pro_first(PRO);         // of them, before the barrier
@@ -860,6 +871,13 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const int R_t = (int)min((int64_t)a.R, a.M - (int64_t)tile * a.R);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
+  auto stamp = [&](int k) {
+    if constexpr (PHASE) {
+      const uint64_t t = __builtin_amdgcn_s_memrealtime();
+      if (lane == 0) a.stamps[(uint64_t)blockIdx.x * kPhaseStamps + k] = t;
+    }
+  };
+  if (wave == 0) stamp(0);
   const int rl = lane / C, cl = lane % C;
   const int gf = groups - 1;                      // full-width column groups
   const int C_last = (int)(nb - (int64_t)gf * C);
@@ -1081,6 +1099,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       if (tid + q * nthr < groups) ((u32x4a*)units_lds)[tid + q * nthr] = ur[q];
   }
   __syncthreads();
+  if (wave == 0) stamp(1);
 #pragma unroll
   for (int d = kFirstUnits; d < kPrefetch; ++d) pf[d] = Pref{0, 0, 0, 0, 0, 0, 0, 0};
 
@@ -1251,6 +1270,13 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // the last column group, by the wave next in turn; its lanes past the last
   // column read zero x and add exactly zero
   if (wave == w_last) process(plast, gf, Ll, std::true_type{});
+  if constexpr (PHASE) {
+    // the wave's sum depends on every unit it decoded: stamp once it exists
+    float s0 = acc[0];
+    asm volatile("" : "+v"(s0));
+    acc[0] = s0;
+    stamp(2 + wave);
+  }
   if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -1266,6 +1292,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       a.y[b * a.ldy + (int64_t)tile * a.R + row] = y;
     }
   }
+  if (wave == 0) stamp(10);
 }
 
 // --------------------------------------------------------- decode export
@@ -1426,15 +1453,16 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
          red;
 }
 
-template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0>
+template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0,
+          bool PHASE = false>
 static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
-  const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO>;
+  const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE>;
   if (shmem > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO>), dim3((unsigned)a.tiles),
-                     dim3(64 * a.waves), shmem, st, a);
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE>),
+                     dim3((unsigned)a.tiles), dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
   return LEECH_OK;
@@ -1454,28 +1482,28 @@ static int prologue_mode(const GemvArgs& a) {
   return per_wave <= 6 ? 2 : per_wave <= 16 ? 1 : 0;
 }
 
-template <int LAYOUT, bool EVEN, int NB, int XPER>
+template <int LAYOUT, bool EVEN, int NB, int XPER, bool PHASE = false>
 static int launch_gemv_pro(const GemvArgs& a, size_t shmem, hipStream_t st) {
   if constexpr (NB == 1 && EVEN && LAYOUT != kNoWeights) {
     switch (prologue_mode(a)) {
-      case 2: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 2>(a, shmem, st);
-      case 1: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 1>(a, shmem, st);
+      case 2: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 2, PHASE>(a, shmem, st);
+      case 1: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 1, PHASE>(a, shmem, st);
       default: break;
     }
   }
-  return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER>(a, shmem, st);
+  return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 0, PHASE>(a, shmem, st);
 }
 
-template <int LAYOUT, bool EVEN, int NB = 1>
+template <int LAYOUT, bool EVEN, int NB = 1, bool PHASE = false>
 static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
   // one activation block per thread when the workgroup's threads cover them
   if (NB > 1 || a.groups * a.C <= 64 * a.waves)
-    return launch_gemv_pro<LAYOUT, EVEN, NB, 1>(a, shmem, st);
-  return launch_gemv_pro<LAYOUT, EVEN, NB, 2>(a, shmem, st);
+    return launch_gemv_pro<LAYOUT, EVEN, NB, 1, PHASE>(a, shmem, st);
+  return launch_gemv_pro<LAYOUT, EVEN, NB, 2, PHASE>(a, shmem, st);
 }
 
 
-template <int LAYOUT, int NB = 1>
+template <int LAYOUT, int NB = 1, bool PHASE = false>
 static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
   GemvArgs a = a0;
   if constexpr (has_exc<LAYOUT>()) {
@@ -1494,8 +1522,8 @@ static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
   if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
   if (LAYOUT == kNoWeights || even_bases(a, LAYOUT))
-    return launch_gemv_as<LAYOUT, true, NB>(a, shmem, st);
-  return launch_gemv_as<LAYOUT, false, NB>(a, shmem, st);
+    return launch_gemv_as<LAYOUT, true, NB, PHASE>(a, shmem, st);
+  return launch_gemv_as<LAYOUT, false, NB, PHASE>(a, shmem, st);
 }
 
 // Rotated launches (Planes14): the LDS of a plain launch plus the f32
@@ -1793,6 +1821,25 @@ int leech_set_prologue_mode(int mode) {
     return set_error(LEECH_E_ARG, "prologue mode must be LEECH_PROLOGUE_AUTO, 0, 1 or 2");
   g_pro_mode.store(mode, std::memory_order_relaxed);
   return LEECH_OK;
+}
+
+int leech_gemv_phases(const leech_layout_desc* desc, const void* d_main, const void* d_side0,
+                      const void* d_side1, const void* d_class_table, const void* d_codewords,
+                      const uint16_t* d_scale, const float centroid[2], const uint16_t* d_x,
+                      float* d_y, uint64_t* d_stamps, void* stream) {
+  clear_error();
+  if (!centroid || !d_stamps) return set_error(LEECH_E_ARG, "NULL argument");
+  if ((uintptr_t)d_stamps & 7) return set_error(LEECH_E_ARG, "misaligned device pointer");
+  GemvArgs a;
+  int rc = gemv_setup(desc, d_main, d_side0, d_side1, d_class_table, d_codewords, d_scale, d_x,
+                      d_y, &a);
+  if (rc) return rc;
+  if (desc->layout != LEECH_PLANES14)
+    return set_error(LEECH_E_LAYOUT, "phase stamps are recorded for the PLANES14 layout");
+  a.cen0 = centroid[0];
+  a.cen1 = centroid[1];
+  a.stamps = d_stamps;
+  return launch_gemv<LEECH_PLANES14, 1, true>(a, (hipStream_t)stream);
 }
 
 int leech_noweights_ctrl(const leech_layout_desc* desc, const uint16_t* d_x, float* d_y,

@@ -264,6 +264,22 @@ def test_rotated_gemv_validates_before_launch():
     assert e.value.code == -3
 
 
+def test_phase_launch_validates_before_launch():
+    """leech_gemv_phases serves Planes14 only and needs its stamp buffer; both
+    are checked on the host (stand-in device pointers, never dereferenced)."""
+    d = P.LayoutDesc()
+    d.layout, d.M, d.Kpad, d.nb = P.GOLAY70, 128, 48, 2
+    d.lane_cols, d.tile_rows = 16, 4
+    fake = 256
+    with pytest.raises(P.LeechError) as e:
+        _lib.gemv_phases(d, fake, fake, fake, fake, fake, fake, (1, 1), fake, fake, fake)
+    assert e.value.code == -2
+    d.layout = P.PLANES14
+    with pytest.raises(P.LeechError) as e:
+        _lib.gemv_phases(d, fake, 0, 0, fake, 0, fake, (1, 1), fake, fake, 0)
+    assert e.value.code == -1
+
+
 def test_rotate_validates_before_launch():
     fake = 256
     for K, Kpad, code in ((0, 24, -3), (48, 24, -3), (65536, 65544, -3)):
