@@ -95,6 +95,9 @@ def parse():
     ap.add_argument("--geometry-sweep", action="store_true",
                     help="only time the candidate tile geometries of the decoder projection "
                          "shapes (Planes14) and print them as one JSON line")
+    ap.add_argument("--geometry-all", action="store_true",
+                    help="with --geometry-sweep: time a broad set of geometries (every lane_cols, "
+                         "tile heights in steps of 4 or 8) on the decoder shapes and 14 more")
     ap.add_argument("--calib-mib", type=int, default=0,
                     help="first run a plain device-to-device copy of this many MiB, 5 times: "
                          "the known-size reference that scales the HBM byte counters")
@@ -984,12 +987,18 @@ def bench_large(args, torch, P, synth):
 GEOMETRY_SHAPES = [(4096, 4104), (1024, 4104), (6144, 4104), (14336, 4104), (28672, 4104),
                    (4096, 14352), (5120, 5136), (1024, 5136), (7168, 5136), (17408, 5136),
                    (34816, 5136), (5120, 17424), (8192, 8208)]
+GEOMETRY_SHAPES_MORE = [(3072, 3096), (2048, 2064), (12288, 12312), (6144, 6168), (10240, 5136),
+                        (20480, 5136), (24576, 4104), (8192, 4104), (4096, 8208), (16384, 4104),
+                        (2560, 5136), (12288, 4104), (3584, 4104), (9216, 4104)]
+# the broad set of --geometry-all: (lane_cols, tile heights)
+GEOMETRY_ALL = {1: [16, 24, 32, 40, 48, 56, 64], 2: [8, 12, 16, 20, 24, 28, 32], 3: [8, 12, 16, 20],
+                4: [4, 8, 12, 16], 8: [4, 8], 16: [4]}
 
 
 def geometry_candidates(M, Kpad, n=6):
-    """The n geometries (lane_cols, tile_rows) of least modelled cost (the
-    library's rule: ceil(tiles / 256) · (units per wave + 3)), plus the
-    power-of-two tile of the same lane_cols."""
+    """The n geometries (lane_cols, tile_rows) of least cost under a simple
+    ranking, ceil(tiles / 256) · (units per wave + 3), plus the power-of-two
+    tile of the same lane_cols."""
     nb = Kpad // 24
     cands = []
     for C in (1, 2, 3, 4, 8, 16):
@@ -1013,7 +1022,9 @@ def bench_geometry(args, torch, P, synth):
     Codes are drawn once (Planes14's time does not depend on them) and tiled
     into each shape; every geometry's y is first checked against the library
     choice's (normalised difference ≤ 2e-3); each timing is a graph replay over
-    ≥ 512 MiB of replicas, geometries interleaved over three rounds, medians."""
+    ≥ 512 MiB of replicas, geometries interleaved over three rounds, medians.
+    --geometry-all times the broad set GEOMETRY_ALL on these shapes and on
+    GEOMETRY_SHAPES_MORE."""
     import numpy as np
     dev = torch.device("cuda:0")
     dcb = P.DeviceCodebook(P.Codebook(12), dev)
@@ -1023,7 +1034,8 @@ def bench_geometry(args, torch, P, synth):
     pgain, pscale = pool.gain.reshape(-1), pool.scale.reshape(-1)
     rng = np.random.default_rng(12)
     res = {}
-    for M, Kpad in GEOMETRY_SHAPES:
+    shapes = GEOMETRY_SHAPES + (GEOMETRY_SHAPES_MORE if args.geometry_all else [])
+    for M, Kpad in shapes:
         t0 = time.time()
         nb = Kpad // 24
         pick = rng.integers(0, pcls.size, M * nb)
@@ -1033,7 +1045,8 @@ def bench_geometry(args, torch, P, synth):
         x = torch.from_numpy(synth.make_activation(Kpad, seed=13, name="geometry")).to(dev)
         y = torch.empty(M, dtype=torch.float32, device=dev)
         lib = P.layout_geometry(M, Kpad)
-        geos = geometry_candidates(M, Kpad)
+        geos = ([(c, r) for c, rs in GEOMETRY_ALL.items() for r in rs] if args.geometry_all
+                else geometry_candidates(M, Kpad))
         if lib not in geos:
             geos.insert(0, lib)
         mats, yref = {}, None
@@ -1173,7 +1186,7 @@ def cpu_model() -> str:
 
 
 def cpu_baseline(inp, seconds):
-    """The oracle as it stands, on the host (the benchmark's CPU plan): (a) decode
+    """The oracle as it stands, on the host: (a) decode
     every block from its fields, form the f64 weights and multiply, and (b)
     the f64 matvec alone on the decoded weights, each repeated for about a
     quarter of `seconds`, once with the BLAS pool held to one thread and once

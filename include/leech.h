@@ -179,9 +179,16 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  * (leech_layout_geometry), which evens out the 256 CUs' work: with
  * L = ceil(tiles / 256) rounds of one tile per CU and a wave taking every 8th
  * unit of its tile, the choice has the least
- * L · 5 + max(L · units per wave, tiles · units per tile / 1664), ties going
- * to more tiles and then to more blocks per unit (4096 × 4104: 4 × 16, i.e.
- * lane_cols × tile_rows; 5120 × 5136: 3 × 20; 8192 × 8208: 2 × 32;
+ * L · 5 + max(L · units per wave, tiles · units per tile / 1792), plus from
+ * three rounds up 1.5 · (L − tiles / 256) · units per wave (the CUs a
+ * partial last round leaves idle), ties going to more blocks per unit and
+ * then to more tiles; where that choice is one round of 9 to 17 units per
+ * wave, it moves to 257..512 tiles (two per CU, which a CU runs at once) of
+ * at least 48 blocks per unit, at most ceil(units per wave / 2) + 1 units per
+ * wave and no more rows per CU (the most blocks per unit, then the fewest
+ * rows per CU, then the most tiles) (4096 × 4104: 4 × 16, i.e. lane_cols ×
+ * tile_rows; 5120 × 5136: 3 × 20; 8192 × 8208: 2 × 32; 6144 × 4104 and
+ * 8192 × 4104: 4 × 16; 34816 × 5136: 2 × 28;
  * 14336 × 4104: 1 × 64).  leech_expand_layout_tiled takes the caller's.
  */
 enum { LEECH_SLOT32 = 0, LEECH_PLANES14 = 1, LEECH_PLANES12X = 2, LEECH_GOLAY70 = 3 };
@@ -334,11 +341,11 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
  * side list (§3.2: Golay70's plain decoder and one that hoists work out of
  * the per-slot path; Planes12x's correction of its five-level blocks).
  *   LEECH_EXC_HOISTED (default): each workgroup first decodes its tile's
- *     exception records densely and keeps each one's contribution in LDS; the
- *     per-block loop then runs the Golay70 decode alone and an exception lane
- *     takes its kept value.
+ *     exception records densely and keeps each one's contribution in LDS as a
+ *     table entry of its own; the per-block loop then runs the layout's own
+ *     decode alone, and an exception lane's lookup yields its kept value.
  *   LEECH_EXC_INLINE: every wave step that holds an exception decodes it in
- *     the loop, beside the Golay70 decode of the other lanes.
+ *     the loop, beside the layout's decode of the other lanes.
  * Both give bit-identical y.  A tile whose exception records exceed the LDS
  * budget is decoded in line either way.  LEECH_E_ARG for another value. */
 enum { LEECH_EXC_HOISTED = 0, LEECH_EXC_INLINE = 1 };
@@ -347,8 +354,8 @@ int leech_set_exception_mode(int mode);
 /* Order in which single (non-batched, non-rotated) GEMVs enqueued from this
  * call on (process-wide) request their weight records, for measurement (§2.3:
  * the kernel streams the records; §3.4 attributes the gap to the DRAM floor
- * largely to latency and occupancy).  Every wave keeps 8 (mode 2: 6) units of
- * 64 blocks in flight; before the workgroup's staging barrier it requests
+ * largely to latency and occupancy).  Every wave keeps 8 (mode 2: 6) units
+ * (tile_rows × lane_cols blocks each) in flight; before the workgroup's staging barrier it requests
  * all 8 (mode 0), 3 (mode 1) or 2 (mode 2) of them, and the rest one per step
  * afterwards.  LEECH_PROLOGUE_AUTO (default) picks by the units a wave
  * streams: ≤ 6 -> 2, ≤ 16 -> 1, more -> 0.  The summation order does not

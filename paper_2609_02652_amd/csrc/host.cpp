@@ -46,34 +46,52 @@ void choose_geometry(int64_t M, int64_t nb, int* C_out, int* R_out) {
   // another through its prefetch ring, so a round lasts at least the units
   // per wave, and the whole launch at least the unit steps of all tiles over
   // what the CUs retire together.  Cost, in unit steps:
-  //     L · 5 + max(L · units per wave, tiles · units per tile / (256 · 6.5))
-  // (5: a tile's staging, ramp and reduction; 6.5 unit steps in flight per
-  // CU), fitted to the per-geometry timings of the decoder projection shapes
-  // (bench --geometry-sweep).  The least cost wins; ties go to more tiles,
-  // then to more blocks per unit.  4096 rows × 171 blocks take 4 columns ×
-  // 16 rows (256 tiles); 5120 rows × 214 or 726 blocks take 3 × 20 (256
-  // tiles, against 160 of 2 × 32: 6.2 against 6.7 µs and 13.1 against
-  // 14.6 µs); 8192 × 342 takes 2 × 32; 14336 × 171 takes 1 × 64.
+  //     L · 5 + max(L · units per wave, tiles · units per tile / (256 · 7))
+  // (5: a tile's staging, ramp and reduction; 7 unit steps in flight per
+  // CU), plus, from three rounds up, 1.5 · (L − tiles / 256) · units per
+  // wave for the CUs a partial last round leaves idle.  The least cost wins;
+  // ties go to more blocks per unit (idle lanes cost issue slots but move no
+  // bytes), then to more tiles.
+  // A CU holds two workgroups at once.  Where the choice is one round of 9
+  // to 17 units per wave, the prefetch ramp is a large part of each wave's
+  // time, and two tiles per CU, each half as long, overlap their ramps: the
+  // choice then moves to 257..512 tiles of at least 48 blocks per unit with
+  // at most half the units per wave (rounded up, plus one) and no more rows
+  // per CU, the most blocks per unit first, then the fewest rows per CU,
+  // then the most tiles.  Fitted to per-geometry timings of 27 shapes from
+  // 2048 to 34816 rows (bench --geometry-sweep --geometry-all): 4096 rows ×
+  // 171 blocks take 4 columns × 16 rows; 5120 rows × 214 or 726 blocks 3 × 20
+  // (256 tiles, against 160 of 2 × 32: 6.3 against 6.7 µs and 12.9 against
+  // 14.7 µs); 8192 × 342 takes 2 × 32; 8192 × 171 and 6144 × 171 take
+  // 4 × 16 (512 and 384 tiles: 6.6 against 7.3 µs for 2 × 32 at 8192 rows);
+  // 34816 × 214 takes 2 × 28 (1244 tiles in 4.9 rounds, against 1088 of
+  // 2 × 32 in 4.25: 23.6 against 24.5 µs); 14336 × 171 takes 1 × 64.
   constexpr int64_t kCUs = 256;
-  constexpr double kTileFixedUnits = 5.0, kUnitsInFlight = 6.5;
+  constexpr double kTileFixedUnits = 5.0, kUnitsInFlight = 7.0, kIdleTail = 1.5;
   static const int kCols[] = {1, 2, 3, 4, 8, 16};
+  auto shape = [&](int C, int R, int64_t& tiles, int64_t& per_wave, int64_t& L) {
+    tiles = (M + R - 1) / R;
+    const int64_t groups = (nb + C - 1) / C;
+    const int64_t waves = std::min<int64_t>(8, groups);
+    per_wave = (groups + waves - 1) / waves;
+    L = (tiles + kCUs - 1) / kCUs;
+    return groups;
+  };
   double best_cost = 0.0;
   int64_t best_tiles = 0;
   int best_lanes = 0, bc = 0, br = 0;
   for (int C : kCols)
     for (int R = 4; R * C <= kWave; R += 4) {
-      const int64_t tiles = (M + R - 1) / R;
-      const int64_t groups = (nb + C - 1) / C;
-      const int64_t waves = std::min<int64_t>(8, groups);
-      const int64_t per_wave = (groups + waves - 1) / waves;
-      const int64_t L = (tiles + kCUs - 1) / kCUs;
-      const double cost = (double)L * kTileFixedUnits +
-                          std::max((double)(L * per_wave),
-                                   (double)tiles * (double)groups / (kCUs * kUnitsInFlight));
+      int64_t tiles, per_wave, L;
+      const int64_t groups = shape(C, R, tiles, per_wave, L);
+      double cost = (double)L * kTileFixedUnits +
+                    std::max((double)(L * per_wave),
+                             (double)tiles * (double)groups / (kCUs * kUnitsInFlight));
+      if (L >= 3) cost += kIdleTail * ((double)L - (double)tiles / kCUs) * (double)per_wave;
       const int lanes = R * C;
       if (bc == 0 || cost < best_cost ||
           (cost == best_cost &&
-           (tiles > best_tiles || (tiles == best_tiles && lanes > best_lanes)))) {
+           (lanes > best_lanes || (lanes == best_lanes && tiles > best_tiles)))) {
         best_cost = cost;
         best_tiles = tiles;
         best_lanes = lanes;
@@ -81,6 +99,34 @@ void choose_geometry(int64_t M, int64_t nb, int* C_out, int* R_out) {
         br = R;
       }
     }
+  int64_t t1, s1, l1;
+  shape(bc, br, t1, s1, l1);
+  if (l1 == 1 && s1 >= 9 && s1 <= 17) {
+    int pc = 0, pr = 0, p_lanes = 0;
+    int64_t p_rows = 0, p_tiles = 0;
+    for (int C : kCols)
+      for (int R = 4; R * C <= kWave; R += 4) {
+        int64_t tiles, per_wave, L;
+        shape(C, R, tiles, per_wave, L);
+        const int lanes = R * C;
+        const int64_t rows = L * R;
+        if (tiles <= kCUs || tiles > 2 * kCUs || lanes < 48 || per_wave > (s1 + 1) / 2 + 1 ||
+            rows > br)
+          continue;
+        if (pc == 0 || lanes > p_lanes || (lanes == p_lanes && rows < p_rows) ||
+            (lanes == p_lanes && rows == p_rows && tiles > p_tiles)) {
+          pc = C;
+          pr = R;
+          p_lanes = lanes;
+          p_rows = rows;
+          p_tiles = tiles;
+        }
+      }
+    if (pc != 0) {
+      bc = pc;
+      br = pr;
+    }
+  }
   *C_out = bc;
   *R_out = br;
 }

@@ -1,9 +1,9 @@
 """GPU parity across tile geometries (lane_cols × tile_rows) and row groups
 that share a tile, through the C ABI.
 
-* Every geometry the kernels serve that the library's choice can reach on the
-  workload shapes (3 × 20, 2 × 28, 2 × 24, 1 × 56, 1 × 60, ...) plus small
-  ones, on a matrix with a ragged last tile and a ragged last column group:
+* Geometries of every lane_cols the kernels serve, the library's choices on
+  the workload shapes among them (3 × 20, 4 × 16, 2 × 32, 1 × 64, 8 × 8, ...),
+  plus small ones, on a matrix with a ragged last tile and a ragged last column group:
   each layout decodes bit-exactly to the drawn points, all four layouts (and
   both exception decoders) give bit-identical y, and y is within the GEMV
   tolerance of the oracle's f64 matvec on every row.

@@ -10,7 +10,8 @@ Each matrix is drawn with its own seed, served as Planes14, decoded on the GPU
 and compared with the drawn points in full (bit-exact), and its GEMV is
 compared with the oracle's f64 matvec on sampled rows, which the oracle
 computes one by one.  These shapes take the geometries (lane_cols × tile_rows)
-1 × 56, 2 × 28, 3 × 20, 4 × 16 and 16 × 4.  A tall matrix with a one-row last
+1 × 64, 2 × 24, 3 × 20, 4 × 16 and 16 × 4; the fused 8B launches 4 × 16 (two
+tiles per CU) and 1 × 64.  A tall matrix with a one-row last
 tile at 1 × 64 exercises the kernel variant whose unit bases are not
 4-aligned, for every layout.
 """

@@ -293,16 +293,21 @@ def test_rotate_validates_before_launch():
 
 def test_geometry_fills_the_gpu():
     """The library's geometry has the least L · 5 + max(L · units per wave,
-    tiles · units per tile / 1664), L = ceil(tiles / 256), ties to more tiles,
-    then to more blocks per unit: 5120-row projections take 256 tiles of
-    3 × 20 rather than 160 of 2 × 32, the other decoder shapes full 64-block
-    units."""
+    tiles · units per tile / 1792), L = ceil(tiles / 256), plus from three
+    rounds up 1.5 · (L − tiles / 256) · units per wave; ties to more blocks per
+    unit, then to more tiles; a choice of one round with 9 to 17 units per
+    wave moves to two tiles per CU of at most half the units per wave (plus
+    one).  5120-row projections take 256 tiles of 3 × 20 rather than 160 of
+    2 × 32; 6144, 7168 and 8192 rows of 171 or 214 blocks take 4 × 16 (two
+    tiles per CU); 34816 rows take 2 × 28 (a fuller last round than 2 × 32);
+    the other decoder shapes full 64-block units."""
     cases = {(1, 24): (1, 64), (64, 24): (16, 4), (768, 1536): (16, 4), (1024, 4104): (16, 4),
              (4096, 4104): (4, 16), (5120, 5136): (3, 20), (5120, 17424): (3, 20),
-             (6144, 4104): (2, 32), (7168, 5136): (2, 32), (8192, 8208): (2, 32),
-             (14336, 4104): (1, 64), (14337, 120): (1, 60), (17408, 5136): (2, 28),
-             (28672, 4104): (1, 64), (34816, 5136): (2, 32), (16384, 16392): (1, 64),
-             (152064, 5136): (1, 64)}
+             (6144, 4104): (4, 16), (7168, 5136): (4, 16), (8192, 8208): (2, 32),
+             (8192, 4104): (4, 16), (4096, 8208): (8, 8), (10240, 5136): (3, 20),
+             (14336, 4104): (1, 64), (14337, 120): (1, 64), (17408, 5136): (2, 24),
+             (28672, 4104): (1, 64), (34816, 5136): (2, 28), (16384, 16392): (1, 64),
+             (152064, 5136): (1, 60)}
     for (M, Kpad), want in cases.items():
         assert P.layout_geometry(M, Kpad) == want, (M, Kpad)
     cb_ = P.Codebook(12)
