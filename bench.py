@@ -6,7 +6,8 @@
 A step is one GEMV y = W x of the workload matrix in the served layout
 (Planes14, 4.80 b/w records + fp16 per-block scales), with W and x resident in
 HBM.  The timed region is exactly K steps, bracketed by a device
-synchronisation on both sides and timed with HIP events on the launch stream.
+synchronisation on both sides and timed with HIP events on the launch stream
+(created without the system-scope fence, which timing does not need).
 The matrix is held in n replicas (same codes, distinct buffers, ≥ 1 GiB in
 all); step j reads replica j mod n.  Right before the timed steps, a replay
 of the replicas the timed region does not read (or, when K leaves fewer than
@@ -245,17 +246,81 @@ def verify_arms(torch, inp, arms, y):
     return res
 
 
+_HIP = None
+
+
+def hip_runtime():
+    """The HIP runtime PyTorch already loaded (looked up by its soname, never
+    loaded a second time), or None."""
+    global _HIP
+    if _HIP is None:
+        import ctypes
+        try:
+            _HIP = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD)
+        except OSError:
+            _HIP = False
+    return _HIP or None
+
+
+class TimingEvent:
+    """A HIP event for timing only: created with hipEventDisableSystemFence,
+    so recording it writes back and invalidates no caches (the kernels between
+    two such events see the caches as they would without them, and the
+    markers' own cost shrinks).  Falls back to torch.cuda.Event where the
+    runtime cannot be looked up; `kind` says which."""
+    FLAGS = 0x20000000  # hipEventDisableSystemFence
+
+    def __init__(self, torch):
+        import ctypes
+        self._c = ctypes
+        self.hip = hip_runtime()
+        if self.hip is None:
+            self.kind = "torch.cuda.Event"
+            self.ev = torch.cuda.Event(enable_timing=True)
+            return
+        self.kind = "hipEvent, no system fence"
+        self.ev = ctypes.c_void_p()
+        rc = self.hip.hipEventCreateWithFlags(ctypes.byref(self.ev), ctypes.c_uint(self.FLAGS))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed: {rc}")
+
+    def record(self, stream):
+        if self.hip is None:
+            self.ev.record(stream)
+            return
+        rc = self.hip.hipEventRecord(self.ev, self._c.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed: {rc}")
+
+    def query(self):
+        if self.hip is None:
+            return self.ev.query()
+        return self.hip.hipEventQuery(self.ev) == 0
+
+    def elapsed_time(self, other):
+        if self.hip is None:
+            return self.ev.elapsed_time(other.ev)
+        ms = self._c.c_float()
+        rc = self.hip.hipEventElapsedTime(self._c.byref(ms), self.ev, other.ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return ms.value
+
+    def __del__(self):
+        if getattr(self, "hip", None) is not None:
+            self.hip.hipEventDestroy(self.ev)
+
+
 def timed_replay(torch, lead, g):
-    """ms of one replay of graph g, timed with HIP events on the current
-    stream.  The device is synchronised first; then `lead` (a graph, or None)
+    """ms of one replay of graph g, timed with HIP events (TimingEvent) on the
+    current stream.  The device is synchronised first; then `lead` (a graph, or None)
     is replayed untimed and the events and g are enqueued behind it without
     waiting, so the device is still busy with `lead` while the host submits
     g: the timed interval holds g's kernels back to back and not the host's
     submission of the graph.  The device is synchronised again before the
     events are read."""
     st = torch.cuda.current_stream()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    e0, e1 = TimingEvent(torch), TimingEvent(torch)
     torch.cuda.synchronize()
     if lead is not None:
         lead.replay()
@@ -292,8 +357,7 @@ def time_arm_stream(torch, arm, steps, leads=2):
     start, length, _ = arm.evict_plan(steps)
     lead = arm.graph(torch, length, start)
     st = torch.cuda.current_stream()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    e0, e1 = TimingEvent(torch), TimingEvent(torch)
     torch.cuda.synchronize()
     for _ in range(leads):
         lead.replay()
@@ -1288,6 +1352,7 @@ def main():
     ev_start, ev_len, between = main_arm.evict_plan(args.steps)
     n_rep = len(main_arm.launchers)
     timed = {"launch": "stream, enqueued ahead" if ahead else "graph",
+             "events": TimingEvent(torch).kind,
              "us_per_gemv_stream": round(ms_stream * 1e3 / args.steps, 3),
              "stream_enqueued_ahead": ahead,
              "us_per_gemv_graph": round(ms_graph * 1e3 / args.steps, 3),

@@ -179,8 +179,8 @@ int leech_fields_from_points(const leech_codebook* cb, int64_t n, const int8_t* 
  * (leech_layout_geometry), which evens out the 256 CUs' work: with
  * L = ceil(tiles / 256) rounds of one tile per CU and a wave taking every 8th
  * unit of its tile, the choice has the least
- * L · 5 + max(L · units per wave, tiles · units per tile / 1792), plus from
- * three rounds up 1.5 · (L − tiles / 256) · units per wave (the CUs a
+ * L · 5 + max(L · units per wave, tiles · units per tile / 1792), plus for
+ * three to six rounds 1.5 · (L − tiles / 256) · units per wave (the CUs a
  * partial last round leaves idle), ties going to more blocks per unit and
  * then to more tiles; where that choice is one round of 9 to 17 units per
  * wave, it moves to 257..512 tiles (two per CU, which a CU runs at once) of

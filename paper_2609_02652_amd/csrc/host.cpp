@@ -48,8 +48,9 @@ void choose_geometry(int64_t M, int64_t nb, int* C_out, int* R_out) {
   // what the CUs retire together.  Cost, in unit steps:
   //     L · 5 + max(L · units per wave, tiles · units per tile / (256 · 7))
   // (5: a tile's staging, ramp and reduction; 7 unit steps in flight per
-  // CU), plus, from three rounds up, 1.5 · (L − tiles / 256) · units per
-  // wave for the CUs a partial last round leaves idle.  The least cost wins;
+  // CU), plus, for three to six rounds, 1.5 · (L − tiles / 256) · units per
+  // wave for the CUs a partial last round leaves idle (over more rounds the
+  // CUs' uneven finishing spreads the last tiles out).  The least cost wins;
   // ties go to more blocks per unit (idle lanes cost issue slots but move no
   // bytes), then to more tiles.
   // A CU holds two workgroups at once.  Where the choice is one round of 9
@@ -65,7 +66,8 @@ void choose_geometry(int64_t M, int64_t nb, int* C_out, int* R_out) {
   // 14.7 µs); 8192 × 342 takes 2 × 32; 8192 × 171 and 6144 × 171 take
   // 4 × 16 (512 and 384 tiles: 6.6 against 7.3 µs for 2 × 32 at 8192 rows);
   // 34816 × 214 takes 2 × 28 (1244 tiles in 4.9 rounds, against 1088 of
-  // 2 × 32 in 4.25: 23.6 against 24.5 µs); 14336 × 171 takes 1 × 64.
+  // 2 × 32 in 4.25: 23.6 against 24.5 µs); 14336 × 171 and 152064 × 214
+  // take 1 × 64.
   constexpr int64_t kCUs = 256;
   constexpr double kTileFixedUnits = 5.0, kUnitsInFlight = 7.0, kIdleTail = 1.5;
   static const int kCols[] = {1, 2, 3, 4, 8, 16};
@@ -87,7 +89,8 @@ void choose_geometry(int64_t M, int64_t nb, int* C_out, int* R_out) {
       double cost = (double)L * kTileFixedUnits +
                     std::max((double)(L * per_wave),
                              (double)tiles * (double)groups / (kCUs * kUnitsInFlight));
-      if (L >= 3) cost += kIdleTail * ((double)L - (double)tiles / kCUs) * (double)per_wave;
+      if (L >= 3 && L <= 6)
+        cost += kIdleTail * ((double)L - (double)tiles / kCUs) * (double)per_wave;
       const int lanes = R * C;
       if (bc == 0 || cost < best_cost ||
           (cost == best_cost &&

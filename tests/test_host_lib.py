@@ -293,8 +293,8 @@ def test_rotate_validates_before_launch():
 
 def test_geometry_fills_the_gpu():
     """The library's geometry has the least L · 5 + max(L · units per wave,
-    tiles · units per tile / 1792), L = ceil(tiles / 256), plus from three
-    rounds up 1.5 · (L − tiles / 256) · units per wave; ties to more blocks per
+    tiles · units per tile / 1792), L = ceil(tiles / 256), plus for three to
+    six rounds 1.5 · (L − tiles / 256) · units per wave; ties to more blocks per
     unit, then to more tiles; a choice of one round with 9 to 17 units per
     wave moves to two tiles per CU of at most half the units per wave (plus
     one).  5120-row projections take 256 tiles of 3 × 20 rather than 160 of
@@ -307,7 +307,7 @@ def test_geometry_fills_the_gpu():
              (8192, 4104): (4, 16), (4096, 8208): (8, 8), (10240, 5136): (3, 20),
              (14336, 4104): (1, 64), (14337, 120): (1, 64), (17408, 5136): (2, 24),
              (28672, 4104): (1, 64), (34816, 5136): (2, 28), (16384, 16392): (1, 64),
-             (152064, 5136): (1, 60)}
+             (152064, 5136): (1, 64), (65536, 8208): (1, 64)}
     for (M, Kpad), want in cases.items():
         assert P.layout_geometry(M, Kpad) == want, (M, Kpad)
     cb_ = P.Codebook(12)
