@@ -9,14 +9,17 @@ HBM.  The timed region is exactly K steps, bracketed by a device
 synchronisation on both sides and timed with HIP events on the launch stream
 (created without the system-scope fence, which timing does not need).
 The matrix is held in n replicas (same codes, distinct buffers, ≥ 1 GiB in
-all); step j reads replica j mod n.  Right before the timed steps, a replay
+all); step j reads replica j mod n.  Right before the timed steps, replays
 of the replicas the timed region does not read (or, when K leaves fewer than
-512 MiB of them, of every replica) streams ≥ 512 MiB, twice the 256 MB
+512 MiB of them, of every replica) stream ≥ 512 MiB, twice the 256 MB
 Infinity Cache, so no replica the timed region reads can still be cached: its
-bytes come from HBM.  The timed steps are enqueued behind that replay without
-waiting for it: K launches one by one when the host has enqueued them all
-before the device reaches the first (checked, and reported), else one graph
-of K launches; the interval then holds the K kernels back to back.  The line
+bytes come from HBM.  The timed steps are enqueued behind those replays
+without waiting for them, and the replays last at least twice (three times
+for single launches) as many launches as the timed region, so the host has
+submitted the timed launches before the device reaches them (checked, and
+reported): K launches one by one when the host has enqueued them all in
+time, else one graph of K launches; the interval then holds the K kernels
+back to back.  The line
 states the timed bytes, the working set and the fewest bytes streamed between
 a replica's previous read and its timed read, both launch forms' times, and
 the same GEMV timed over one whole ≥ 1 GiB cycle of replicas beside it.
@@ -43,16 +46,23 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published peak
 REPLICA_BYTES = 1 << 30        # working set per arm: 4× the 256 MB Infinity Cache
 EVICT_BYTES = 512 << 20        # streamed right before a timed replay: 2× that cache
 # rotated arms that mix the two forms: the activation is rotated inside the
-# GEMV's prologue up to this K and this many workgroups (each workgroup redoes
-# the whole transform, which pays while K is small and the workgroups few), by
-# the separate rotation kernel otherwise
+# GEMV's prologue up to this K, this many workgroups and from this many units
+# per wave (each workgroup redoes the whole transform, which pays while K is
+# small, the workgroups few, and each wave's stream long enough to hide it
+# behind the record loads in flight), by the separate rotation kernel
+# otherwise (bench layer_8b.rotation_sites measures both forms at every site)
 ROT_IN_KERNEL_MAX_K = 5120
 ROT_IN_KERNEL_MAX_TILES = 512
+ROT_IN_KERNEL_MIN_UNITS = 16
 
 
 def rotate_in_kernel(m, K):
-    tiles = -(-m.desc.M // m.desc.tile_rows)
-    return K <= ROT_IN_KERNEL_MAX_K and tiles <= ROT_IN_KERNEL_MAX_TILES
+    d = m.desc
+    tiles = -(-d.M // d.tile_rows)
+    groups = -(-d.nb // d.lane_cols)
+    units = -(-groups // min(8, groups))
+    return (K <= ROT_IN_KERNEL_MAX_K and tiles <= ROT_IN_KERNEL_MAX_TILES
+            and units >= ROT_IN_KERNEL_MIN_UNITS)
 ARMS = ["planes14", "slot32", "planes12x", "planes12x_inline", "golay70", "golay70_inline",
         "fp16", "noweights"]
 CONFIGS = {"c1_768x1536": (768, 1536), "c2_4096x4096": (4096, 4096),
@@ -311,21 +321,37 @@ class TimingEvent:
             self.hip.hipEventDestroy(self.ev)
 
 
-def timed_replay(torch, lead, g):
+_LAST_AHEAD = [True]
+
+
+def lead_reps(steps, lead_len, factor=2):
+    """Replays of a lead graph of lead_len launches to put ahead of a timed
+    region of `steps` launches: the device then works through at least
+    factor × steps launches before it reaches the timed region, time in which
+    the host submits the timed launches (a cold graph's submission can take
+    longer than the device takes to run its kernels)."""
+    return max(1, -(-factor * steps // max(1, lead_len)))
+
+
+def timed_replay(torch, lead, g, reps=2):
     """ms of one replay of graph g, timed with HIP events (TimingEvent) on the
-    current stream.  The device is synchronised first; then `lead` (a graph, or None)
-    is replayed untimed and the events and g are enqueued behind it without
-    waiting, so the device is still busy with `lead` while the host submits
-    g: the timed interval holds g's kernels back to back and not the host's
-    submission of the graph.  The device is synchronised again before the
-    events are read."""
+    current stream.  The device is synchronised first; then `lead` (a graph,
+    or None) is replayed `reps` times untimed and the events and g are
+    enqueued behind it without waiting, so the device is still busy with the
+    lead while the host submits g: the timed interval holds g's kernels back
+    to back and not the host's submission of the graph.  Whether the host had
+    submitted all of g before the device reached the first event is kept in
+    _LAST_AHEAD.  The device is synchronised again before the events are
+    read."""
     st = torch.cuda.current_stream()
     e0, e1 = TimingEvent(torch), TimingEvent(torch)
     torch.cuda.synchronize()
     if lead is not None:
-        lead.replay()
+        for _ in range(reps):
+            lead.replay()
     e0.record(st)
     g.replay()
+    _LAST_AHEAD[0] = not e0.query()
     e1.record(st)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1)
@@ -335,31 +361,37 @@ def time_arm(torch, arm, steps):
     """ms for `steps` GEMVs: one replay of a graph holding exactly `steps`
     launches (replicas 0, 1, …), timed with HIP events on the stream the
     kernels run on, between device synchronisations.  It is enqueued right
-    behind the replay of arm.evict_plan(steps), which streams the replicas
-    the timed region does not read (≥ 512 MiB, twice the Infinity Cache), so
-    that the timed replicas are read from HBM; an arm without weight bytes
-    leads with a replay of its own graph."""
+    behind replays of arm.evict_plan(steps), which streams the replicas the
+    timed region does not read (≥ 512 MiB, twice the Infinity Cache), so that
+    the timed replicas are read from HBM, and which keeps the device busy for
+    at least twice the timed launches while the host submits them; an arm
+    without weight bytes leads with replays of its own graph.  The timed graph
+    is replayed once before the lead: a graph's first replay after other work
+    runs its kernels about 0.5 µs slower each, which the timed replay should
+    not carry."""
     g = arm.graph(torch, steps)
-    lead = g
+    lead, length = g, steps
     if arm.served_bytes:
         start, length, _ = arm.evict_plan(steps)
         lead = arm.graph(torch, length, start)
-    return timed_replay(torch, lead, g)
+    g.replay()
+    return timed_replay(torch, lead, g, lead_reps(steps, length))
 
 
-def time_arm_stream(torch, arm, steps, leads=2):
+def time_arm_stream(torch, arm, steps):
     """ms for `steps` GEMVs launched one by one on the stream (no graph),
-    enqueued behind `leads` replays of the eviction graph of
-    arm.evict_plan(steps), and whether every launch was enqueued before the
-    device reached the timed region (the first event still pending when the
-    host had enqueued the last launch): then the interval holds the kernels
-    back to back, neither the host's launch calls nor a graph's start."""
+    enqueued behind replays of the eviction graph of arm.evict_plan(steps)
+    (at least three times the timed launches), and whether every launch was
+    enqueued before the device reached the timed region (the first event
+    still pending when the host had enqueued the last launch): then the
+    interval holds the kernels back to back, neither the host's launch calls
+    nor a graph's start."""
     start, length, _ = arm.evict_plan(steps)
     lead = arm.graph(torch, length, start)
     st = torch.cuda.current_stream()
     e0, e1 = TimingEvent(torch), TimingEvent(torch)
     torch.cuda.synchronize()
-    for _ in range(leads):
+    for _ in range(max(2, lead_reps(steps, length, 3))):
         lead.replay()
     e0.record(st)
     arm.run(steps)
@@ -374,7 +406,7 @@ def cycle_us(torch, arm, replays=3):
     of `replays` timed replays, each led by an untimed one."""
     n = len(arm.launchers)
     g = arm.graph(torch, n)
-    out = [timed_replay(torch, g, g) * 1e3 / n for _ in range(replays)]
+    out = [timed_replay(torch, g, g, lead_reps(n, n)) * 1e3 / n for _ in range(replays)]
     return statistics.median(out)
 
 
@@ -418,14 +450,14 @@ def prologue_table(args, torch, P, arm):
         for m in res:
             P.set_prologue_mode(P.PROLOGUE_AUTO if m == "auto" else m)
             arm._graphs.clear()
-            start, length, _ = arm.evict_plan(k)
-            graphs[m] = (arm.graph(torch, length, start), arm.graph(torch, k))
+            start, len_ev, _ = arm.evict_plan(k)
+            graphs[m] = (arm.graph(torch, len_ev, start), arm.graph(torch, k))
         arm._graphs.clear()
     finally:
         P.set_prologue_mode(P.PROLOGUE_AUTO)
     for _ in range(5):
         for m, (ev, g) in graphs.items():
-            res[m].append(timed_replay(torch, ev, g) * 1e3 / k)
+            res[m].append(timed_replay(torch, ev, g, lead_reps(k, len_ev)) * 1e3 / k)
     del graphs
     return {str(m): round(statistics.median(v), 3) for m, v in res.items()}
 
@@ -439,8 +471,9 @@ def phase_table(torch, P, arm, x, y, steps=20):
     launch's last store and the next one's first workgroup start; the spread
     of workgroup starts; and, per workgroup (median over workgroups), the
     prologue (start to barrier), the loop (barrier to the last wave's last
-    unit) and the tail (to the last store); the event-timed µs per launch and
-    the counter rate it implies beside them."""
+    unit) and the tail (to the last store); beside them the event-timed µs per
+    launch, the stamped span of all launches, and what the event window holds
+    beyond it (its markers and the graph's start)."""
     import numpy as np
     mats = arm.mats
     n = len(mats)
@@ -457,21 +490,22 @@ def phase_table(torch, P, arm, x, y, steps=20):
     start, length, _ = arm.evict_plan(steps)
     lead = arm.graph(torch, length, start)
     g.replay()
-    ms = timed_replay(torch, lead, g)
+    ms = timed_replay(torch, lead, g, lead_reps(steps, length))
     s = st.cpu().numpy().astype(np.float64)
     del g
     t0, t1, t10 = s[:, :, 0], s[:, :, 1], s[:, :, 10]
     tw = s[:, :, 2:2 + waves].max(axis=2)
     starts, ends = t0.min(axis=1), t10.max(axis=1)
     span_ticks = ends[-1] - starts[0]
-    mhz = span_ticks / (ms * 1e3) if ms > 0 else float("nan")
-    # ticks to µs at the rate that makes the stamped span of the replay equal
-    # its event-timed span (the counter is nominally 100 MHz)
-    us = lambda v: round(float(v) / mhz, 3)  # noqa: E731
+    # the real-time counter runs at 100 MHz; the event-timed interval also
+    # holds the two event markers and the first launch's start, which the
+    # stamps do not: their difference is the window's own cost
+    us = lambda v: round(float(v) / 100.0, 3)  # noqa: E731
     med = lambda v: us(np.median(v))  # noqa: E731
     return {"launches": steps, "workgroups": tiles, "waves": waves,
             "event_us_per_launch": round(ms * 1e3 / steps, 3),
-            "counter_MHz_implied": round(float(mhz), 2),
+            "stamped_us_first_start_to_last_store": us(span_ticks),
+            "event_window_minus_stamped_us": round(ms * 1e3 - span_ticks / 100.0, 3),
             "gap_between_launches_us": med(starts[1:] - ends[:-1]),
             "workgroup_start_spread_us": med(t0.max(axis=1) - starts),
             "prologue_us": med(np.median(t1 - t0, axis=1)),
@@ -1345,6 +1379,7 @@ def main():
     # the K launches one by one behind a lead replay, when the host enqueues
     # them all before the device reaches them; else one graph of K launches
     ms_graph = time_arm(torch, main_arm, args.steps)
+    graph_ahead = _LAST_AHEAD[0]
     ms_stream, ahead = time_arm_stream(torch, main_arm, args.steps)
     ms = ms_stream if ahead else ms_graph
     us = ms * 1e3 / args.steps
@@ -1356,6 +1391,7 @@ def main():
              "us_per_gemv_stream": round(ms_stream * 1e3 / args.steps, 3),
              "stream_enqueued_ahead": ahead,
              "us_per_gemv_graph": round(ms_graph * 1e3 / args.steps, 3),
+             "graph_enqueued_ahead": graph_ahead,
              "timed_bytes": args.steps * main_arm.served_bytes,
              "working_set_bytes": n_rep * main_arm.served_bytes,
              "evict_replay": {"first_replica": ev_start, "launches": ev_len,
