@@ -457,6 +457,7 @@ def prologue_table(args, torch, P, arm):
         P.set_prologue_mode(P.PROLOGUE_AUTO)
     for _ in range(5):
         for m, (ev, g) in graphs.items():
+            g.replay()
             res[m].append(timed_replay(torch, ev, g, lead_reps(k, len_ev)) * 1e3 / k)
     del graphs
     return {str(m): round(statistics.median(v), 3) for m, v in res.items()}
