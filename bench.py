@@ -914,10 +914,13 @@ def bench_transcode(torch, P, dcb, parts, dev):
 
 def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
     """Batched GEMV (§6 "Batching") on the bench workload in Planes14: µs per
-    launch of Y = W X for B activations (each block decoded once for up to 8
-    of them), walking the same replicas as the Planes14 arm; beside it the
-    FP16 weights through the library GEMM (torch.matmul, hipBLASLt) on the
-    same B, as the batched FP16 reference."""
+    launch of Y = W X for B activations (each block decoded once for up to 16
+    of them), walking the same replicas as the Planes14 arm, with the
+    library's default products (matrix cores where tile_rows is a multiple of
+    16) and, for B > 1, with v_dot2 per activation (dot2_us); the largest
+    normalised difference of Y[0] and Y[B-1] from their single GEMVs; beside
+    it the FP16 weights through the library GEMM (torch.matmul, hipBLASLt) on
+    the same B, as the batched FP16 reference."""
     import numpy as np
     dev = torch.device("cuda:0")
     p14 = arms["planes14"]
@@ -929,9 +932,25 @@ def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
         X = torch.from_numpy(np.stack([synth.make_activation(inp.K, seed=50 + b, name="bench-batch")
                                        for b in range(B)])).to(dev)
         Y = torch.empty((B, inp.M), dtype=torch.float32, device=dev)
+        leech[0].gemv_batch(X, Y)
+        diff = 0.0
+        for b in {0, B - 1}:
+            y1 = leech[0].gemv(X[b].contiguous())
+            diff = max(diff, float((Y[b] - y1).abs().max() / y1.abs().max()))
         us = replay_us(torch, lambda i: leech[i % reps].gemv_batch(X, Y), args.layer_steps)
+        mx = B > 1 and leech[0].desc.tile_rows % 16 == 0
         row = {"us": round(us, 2), "us_per_vector": round(us / B, 3),
-               "weight_GBps": round(p14.served_bytes / (us * 1e-6) / 1e9, 1)}
+               "weight_GBps": round(p14.served_bytes / (us * 1e-6) / 1e9, 1),
+               "products": "mfma" if mx else "dot2", "max_norm_diff_vs_single": diff}
+        if B > 1:
+            P.set_batch_mode(P.BATCH_DOT2)
+            try:
+                us_d = replay_us(torch, lambda i: leech[i % reps].gemv_batch(X, Y),
+                                 args.layer_steps)
+            finally:
+                P.set_batch_mode(P.BATCH_AUTO)
+            row["dot2_us"] = round(us_d, 2)
+            row["dot2_vs_default"] = round(us_d / us, 3)
         if fp is not None:
             Ws = fp.mats
             Xt = X.t().contiguous()

@@ -309,8 +309,11 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
  * launch and multiplied with up to 16 activations staged in LDS; larger
  * batches run in chunks of 16 (fewer where Kpad leaves too little LDS: 16
  * activations fit up to about Kpad = 4,600, 8 up to about 9,200, the exact
- * bound depending on the column groups' rounding).  Every
- * Y[b] is bit-identical to leech_gemv on X[b].  batch > 1 serves
+ * bound depending on the column groups' rounding).  Products as
+ * leech_set_batch_mode selects: on the matrix cores (the default where
+ * tile_rows is a multiple of 16) Y[b] is within rounding of leech_gemv on X[b]
+ * and a single vector left after the 16-wide chunks still runs 2 wide; with
+ * v_dot2 Y[b] is bit-identical to leech_gemv on X[b].  batch > 1 serves
  * LEECH_PLANES14 (LEECH_E_LAYOUT otherwise) and needs ldx ≥ Kpad, ldx a
  * multiple of 8 and ldy ≥ M (LEECH_E_ARG); batch = 1 is leech_gemv.  Other
  * arguments as leech_gemv. */
@@ -350,6 +353,19 @@ int leech_gemv_grouped(const leech_layout_desc* desc, const void* d_main, const 
  * budget is decoded in line either way.  LEECH_E_ARG for another value. */
 enum { LEECH_EXC_HOISTED = 0, LEECH_EXC_INLINE = 1 };
 int leech_set_exception_mode(int mode);
+
+/* Products of leech_gemv_batch calls with batch > 1 enqueued from this call on
+ * (process-wide; §6 "Batching").  LEECH_BATCH_AUTO (default): where tile_rows
+ * is a multiple of 16, each decoded block meets its activations on the matrix
+ * cores (16×16×32 binary16 products with f32 accumulation, one block's 24
+ * products per output, so the block's scale and class factor still multiply
+ * its f32 dot product); Y[b] is then within rounding of leech_gemv on X[b]
+ * (the matrix core sums a block's products in its own order) and
+ * bit-identical for a given X[b] whatever the batch size or X[b]'s position.
+ * Other geometries, and LEECH_BATCH_DOT2: v_dot2 per activation, Y[b]
+ * bit-identical to leech_gemv on X[b].  LEECH_E_ARG for another value. */
+enum { LEECH_BATCH_AUTO = 0, LEECH_BATCH_DOT2 = 1 };
+int leech_set_batch_mode(int mode);
 
 /* Order in which single (non-batched, non-rotated) GEMVs enqueued from this
  * call on (process-wide) request their weight records, for measurement (§2.3:

@@ -15,13 +15,15 @@ from ._lib import (GOLAY70, LAYOUT_NAMES, LAYOUTS, PLANES12X, PLANES14, SLOT32, 
                    LayoutDesc, LeechError, expand_layout, host_decode_layout, index_decode,
                    index_encode, layout_geometry, layout_scales, planes14_desc,
                    set_exception_mode,
-                   EXC_HOISTED, EXC_INLINE, set_prologue_mode, PROLOGUE_AUTO)
+                   EXC_HOISTED, EXC_INLINE, set_prologue_mode, PROLOGUE_AUTO,
+                   set_batch_mode, BATCH_AUTO, BATCH_DOT2)
 
 __all__ = ["Codebook", "DeviceCodebook", "LeechMatrix", "LayoutDesc", "LeechError", "LAYOUTS",
            "LAYOUT_NAMES", "SLOT32", "PLANES14", "PLANES12X", "GOLAY70", "expand_layout",
            "host_decode_layout", "layout_scales", "fp16_gemv", "noweights_ctrl", "rotate_x",
            "index_encode", "index_decode", "planes14_desc", "layout_geometry", "set_exception_mode",
-           "EXC_HOISTED", "EXC_INLINE", "set_prologue_mode", "PROLOGUE_AUTO"]
+           "EXC_HOISTED", "EXC_INLINE", "set_prologue_mode", "PROLOGUE_AUTO",
+           "set_batch_mode", "BATCH_AUTO", "BATCH_DOT2"]
 
 
 def _torch():
@@ -142,7 +144,8 @@ class LeechMatrix:
 
     def gemv_batch(self, X, Y=None, centroids=(1.0, 1.0), stream=None):
         """Y[b] = W X[b]: X fp16 [B, Kpad] device tensor (row stride a multiple
-        of 8), Y f32 [B, M]; each block decoded once for up to 8 activations."""
+        of 8), Y f32 [B, M]; each block decoded once for up to 16 activations,
+        multiplied on the matrix cores or with v_dot2 (set_batch_mode)."""
         torch = _torch()
         if X.dtype != torch.float16 or X.dim() != 2 or X.shape[1] != self.Kpad or X.stride(1) != 1:
             raise ValueError("X must be an fp16 [B, Kpad] tensor with unit column stride")

@@ -29,8 +29,8 @@ EXPORTS = ["leech_last_error", "leech_codebook_build", "leech_codebook_free",
            "leech_fp16_gemv_ref", "leech_noweights_ctrl", "leech_rotate_x",
            "leech_index_encode", "leech_index_decode", "leech_planes14_desc",
            "leech_transcode_planes14", "leech_set_exception_mode", "leech_gemv_batch",
-           "leech_gemv_rotated", "leech_set_prologue_mode", "leech_expand_layout_tiled",
-           "leech_layout_geometry", "leech_gemv_phases"]
+           "leech_gemv_rotated", "leech_set_prologue_mode", "leech_set_batch_mode",
+           "leech_expand_layout_tiled", "leech_layout_geometry", "leech_gemv_phases"]
 
 
 class LeechError(RuntimeError):
@@ -96,6 +96,7 @@ def _load() -> C.CDLL:
         "leech_transcode_planes14": (I, [C.POINTER(LayoutDesc), P, P, P, P, P]),
         "leech_set_exception_mode": (I, [I]),
         "leech_set_prologue_mode": (I, [I]),
+        "leech_set_batch_mode": (I, [I]),
         "leech_gemv_batch": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, P, I, P, I64, P, I64,
                                  P]),
         "leech_gemv_rotated": (I, [C.POINTER(LayoutDesc), P, P, P, P, P, P, I, P, P, I64, P, P,
@@ -344,6 +345,16 @@ EXC_HOISTED, EXC_INLINE = 0, 1
 def set_exception_mode(mode: int) -> None:
     """Process-wide: how Golay70 GEMVs enqueued afterwards decode exceptions."""
     check(lib.leech_set_exception_mode(mode))
+
+
+BATCH_AUTO, BATCH_DOT2 = 0, 1
+
+
+def set_batch_mode(mode: int) -> None:
+    """Process-wide: the products of batched GEMVs enqueued afterwards
+    (BATCH_AUTO: matrix cores where tile_rows is a multiple of 16; BATCH_DOT2:
+    v_dot2, bit-identical to single GEMVs)."""
+    check(lib.leech_set_batch_mode(mode))
 
 
 PROLOGUE_AUTO = -1

@@ -636,6 +636,33 @@ __device__ __forceinline__ float row_sum(float v, int C) {
   return v;
 }
 
+// Row sum of the column-placed lanes of a matrix-core launch: row r's C ≤ 4
+// lanes are r, r + R, r + 2R, r + 3R, fetched by ds_bpermute; lane r (c = 0)
+// gets v0 (C = 1), v0 + v1, (v0 + v1) + v2 or (v0 + v1) + (v2 + v3).  Every
+// lane is active here.
+__device__ __forceinline__ float row_sum_cols(float v, int C, int R) {
+  const int l = (int)(threadIdx.x & 63u);
+  auto at = [&](int c) {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_ds_bpermute(((l + c * R) & 63) << 2, __builtin_bit_cast(int, v)));
+  };
+  if (C == 1) return v;
+  const float s01 = v + at(1);
+  if (C == 2) return s01;
+  if (C == 3) return s01 + at(2);
+  return s01 + (at(2) + at(3));
+}
+
+// One 16×16×32 binary16 matrix-core product (f32 accumulate) on operands held
+// as four pair words a lane: lane l holds k = 8·(l / 16) .. + 7 of row l % 16
+// of A and of column l % 16 of B; D row 4·(l / 16) + i, column l % 16 comes
+// back in d[i].
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ f32x4a mfma16(u32x4a a, u32x4a b, f32x4a d) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, a),
+                                                __builtin_bit_cast(half8_t, b), d, 0, 0, 0);
+}
+
 // ------------------------------------------------------- fused rotation
 // The activation rotation (blockwise Walsh–Hadamard, §2.3, §6) done by each
 // GEMV workgroup in its prologue, while its first record loads are in flight:
@@ -830,6 +857,21 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // NB: batch width (1, 2, 4, 8 or 16).  Each decoded block is multiplied with
 // NB activations (NB > 1: Planes14), in the same order as a single GEMV, so
 // every output vector is bit-identical to that activation's own GEMV.
+// MX (NB > 1, tile_rows a multiple of 16): the products go through the matrix
+// cores instead.  Lanes are placed by column (lane c·R + r holds block (r, c)
+// of the unit, R = tile_rows), so each 16-lane group of a wave holds blocks of
+// one block column.  The decoded block is the B operand (column l % 16, its
+// 24 values over three 16×16×32 products); A is block-diagonal: row 4q + i
+// carries activation i's 8 values of group q's column in group q's k range and
+// zeros elsewhere.  D row 4q + i, column n is then the dot product of lane
+// 16q + n's own block with activation i, back in that lane's d[i]: four
+// activations per three products, no sum across blocks, so the block's scale
+// and class factor still multiply its f32 dot product.  The matrix core sums
+// the 24 products in its own order: outputs are within rounding of the
+// single GEMV's and bit-identical across batch widths (activation b always
+// sits in row b mod 4 of product set b / 4).  A lane of group q that carries
+// no activation (row group other than q, or an activation past NB) reads a
+// zero block staged after the activations.
 // XPER: activation blocks each thread stages through registers in the ordered
 // prologue (1 when the workgroup's threads cover every block, else 2; more
 // blocks go through the unordered loop first).
@@ -841,8 +883,10 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // workgroup (lane 0 of the stamping wave, a vector store each); the work is
 // the plain launch's.
 template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false, int PRO = 0,
-          bool PHASE = false>
+          bool PHASE = false, bool MX = false>
 __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
+  static_assert(!MX || (NB > 1 && LAYOUT == LEECH_PLANES14 && !ROT && !PHASE),
+                "matrix-core products serve batched Planes14 launches");
   constexpr int kPrefetch = pro_prefetch(PRO);        // units in flight per wave
   constexpr int kFirstUnits = pro_first(PRO);         // of them, before the barrier
   constexpr bool kRamp = kFirstUnits < kPrefetch;
@@ -856,7 +900,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
   const int xblocks = groups * C;
   uint32_t* xs = (uint32_t*)xbase;                                 // NB × xblocks × 12 x pairs
-  uint8_t* p = xbase + (size_t)NB * xblocks * 48;
+  uint8_t* p = xbase + (size_t)(NB * xblocks + (MX ? 1 : 0)) * 48;  // MX: and a zero block
   uint32_t* cws = (uint32_t*)p;                                    // Golay70: 128 words
   u32x2a* p14t = (u32x2a*)(p + 128 * 4);                           // Golay70: 512 tables
   if constexpr (LAYOUT == LEECH_GOLAY70) p += kG70LdsBytes;
@@ -878,10 +922,10 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   };
   if (wave == 0) stamp(0);
-  const int rl = lane / C, cl = lane % C;
+  const int rl = MX ? lane % a.R : lane / C, cl = MX ? lane / a.R : lane % C;
   const int gf = groups - 1;                      // full-width column groups
   const int C_last = (int)(nb - (int64_t)gf * C);
-  const bool row_ok = rl < R_t, last_ok = row_ok && cl < C_last;
+  const bool row_ok = rl < R_t && (!MX || cl < C), last_ok = row_ok && cl < C_last;
   constexpr uint32_t S = Stride<LAYOUT>::v;
   // 24-bit products: a 64-bit multiply-add chosen for these would read an
   // undefined high half that may sit in a register with a load in flight, and
@@ -928,7 +972,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // (a batched launch stages all its activations here: vector b's blocks
   // follow vector b − 1's, zero past nb and for vectors past nbatch)
   if constexpr (!ROT)
-  for (int j = NB == 1 ? tid + kXPer * nthr : tid; j < NB * xblocks; j += nthr) {
+  for (int j = NB == 1 ? tid + kXPer * nthr : tid; j < NB * xblocks + (MX ? 1 : 0); j += nthr) {
     const int b = NB == 1 ? 0 : j / xblocks, jb = j - b * xblocks;
     if (jb < nb && b < a.nbatch) {
       store_x_block(load_x_block(a.x + b * a.ldx + 24 * (int64_t)jb), xs + 12 * j);
@@ -1176,9 +1220,47 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   float acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = 0.0f;
+  // MX: the A operand's LDS byte address for product set s is
+  // x_on · (unit's x offset) + x_off[s]: activation 4s + m % 4 of the group's
+  // column for a lane on the diagonal (row group m / 4 = its group q, the
+  // activation below NB, a column of the unit), else the zero block
+  constexpr int kSets = MX ? (NB + 3) / 4 : 1;
+  uint32_t x_on = 0u, x_off[kSets];
+  if constexpr (MX) {
+    const int m = lane & 15, q = lane >> 4;
+    const uint32_t x0 = (uint32_t)(xbase - smem);
+    const uint32_t zero = x0 + (uint32_t)(NB * xblocks * 48);
+    const bool on = (m >> 2) == q && (m & 3) < NB && cl < C;
+    x_on = on ? 1u : 0u;
+#pragma unroll
+    for (int s = 0; s < kSets; ++s)
+      x_off[s] = on ? x0 + (uint32_t)(((4 * s + (m & 3)) * xblocks + cl) * 48) : zero;
+  }
   // One unit: decode slot p for unit g and accumulate.  LAST: the last
   // column group, whose stand-in lanes (past the last column) must add zero.
   auto process = [&](const Pref& pr, int g, const Lane& L, auto last) {
+    if constexpr (MX) {
+      uint32_t h[12], e16;
+      LdsEntry te;
+      decode_block<LAYOUT>(pr, tile, tab, tab14, cw, side, h, e16, te);
+      const float sf = (float)as_half(pr.scale) * te.factor;
+      const uint32_t ub = (uint32_t)(g * (C * 48));
+      const u32x4a w0 = {h[0], h[1], h[2], h[3]}, w1 = {h[4], h[5], h[6], h[7]},
+                   w2 = {h[8], h[9], h[10], h[11]};
+#pragma unroll
+      for (int s = 0; s < kSets; ++s) {
+        const u32x4a* xa =
+            (const u32x4a*)__builtin_assume_aligned(smem + (__umul24(x_on, ub) + x_off[s]), 16);
+        f32x4a d = {0.0f, 0.0f, 0.0f, 0.0f};
+        d = mfma16(xa[0], w0, d);
+        d = mfma16(xa[1], w1, d);
+        d = mfma16(xa[2], w2, d);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (4 * s + i < NB) acc[4 * s + i] = __builtin_fmaf(sf, d[i], acc[4 * s + i]);
+      }
+      return;
+    }
     const u32x4a* xp = (const u32x4a*)(x_lane + g * (C * 48));
     const u32x4a x0 = xp[0], x1 = xp[1], x2 = xp[2];
     const uint32_t xw[12] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w,
@@ -1280,7 +1362,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const float v = row_sum(acc[b], C);
+    const float v = MX ? row_sum_cols(acc[b], C, a.R) : row_sum(acc[b], C);
     if (cl == 0 && rl < R_t) red[(b * waves + wave) * 64 + rl] = v;
   }
   __syncthreads();
@@ -1444,24 +1526,25 @@ static bool even_bases(const GemvArgs& a, int layout) {
   return (rows_last * a.C * stride) % 4 == 0;
 }
 
-template <int LAYOUT, int NB = 1>
+template <int LAYOUT, int NB = 1, bool MX = false>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
   const size_t red = red_in_x(NB, a.groups * a.C, a.waves) ? 0 : (size_t)NB * a.waves * 64 * 4;
   const size_t table = LAYOUT == kNoWeights ? 0 : (a.tab2 ? 2 : 1) * (size_t)a.tab_bytes;
-  return table + (size_t)NB * a.groups * a.C * 48 + (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
+  return table + ((size_t)NB * a.groups * a.C + (MX ? 1 : 0)) * 48 +
+         (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
          red;
 }
 
 template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0,
-          bool PHASE = false>
+          bool PHASE = false, bool MX = false>
 static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
-  const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE>;
+  const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>;
   if (shmem > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE>),
+  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>),
                      dim3((unsigned)a.tiles), dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
@@ -1482,8 +1565,9 @@ static int prologue_mode(const GemvArgs& a) {
   return per_wave <= 6 ? 2 : per_wave <= 16 ? 1 : 0;
 }
 
-template <int LAYOUT, bool EVEN, int NB, int XPER, bool PHASE = false>
+template <int LAYOUT, bool EVEN, int NB, int XPER, bool PHASE = false, bool MX = false>
 static int launch_gemv_pro(const GemvArgs& a, size_t shmem, hipStream_t st) {
+  if constexpr (MX) return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 0, false, true>(a, shmem, st);
   if constexpr (NB == 1 && EVEN && LAYOUT != kNoWeights) {
     switch (prologue_mode(a)) {
       case 2: return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 2, PHASE>(a, shmem, st);
@@ -1494,16 +1578,16 @@ static int launch_gemv_pro(const GemvArgs& a, size_t shmem, hipStream_t st) {
   return launch_gemv_kernel<LAYOUT, EVEN, NB, XPER, false, 0, PHASE>(a, shmem, st);
 }
 
-template <int LAYOUT, bool EVEN, int NB = 1, bool PHASE = false>
+template <int LAYOUT, bool EVEN, int NB = 1, bool PHASE = false, bool MX = false>
 static int launch_gemv_as(const GemvArgs& a, size_t shmem, hipStream_t st) {
   // one activation block per thread when the workgroup's threads cover them
   if (NB > 1 || a.groups * a.C <= 64 * a.waves)
-    return launch_gemv_pro<LAYOUT, EVEN, NB, 1, PHASE>(a, shmem, st);
-  return launch_gemv_pro<LAYOUT, EVEN, NB, 2, PHASE>(a, shmem, st);
+    return launch_gemv_pro<LAYOUT, EVEN, NB, 1, PHASE, MX>(a, shmem, st);
+  return launch_gemv_pro<LAYOUT, EVEN, NB, 2, PHASE, MX>(a, shmem, st);
 }
 
 
-template <int LAYOUT, int NB = 1, bool PHASE = false>
+template <int LAYOUT, int NB = 1, bool PHASE = false, bool MX = false>
 static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
   GemvArgs a = a0;
   if constexpr (has_exc<LAYOUT>()) {
@@ -1518,12 +1602,12 @@ static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
       }
     }
   }
-  const size_t shmem = gemv_lds_bytes<LAYOUT, NB>(a);
+  const size_t shmem = gemv_lds_bytes<LAYOUT, NB, MX>(a);
   if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
   if (LAYOUT == kNoWeights || even_bases(a, LAYOUT))
-    return launch_gemv_as<LAYOUT, true, NB, PHASE>(a, shmem, st);
-  return launch_gemv_as<LAYOUT, false, NB, PHASE>(a, shmem, st);
+    return launch_gemv_as<LAYOUT, true, NB, PHASE, MX>(a, shmem, st);
+  return launch_gemv_as<LAYOUT, false, NB, PHASE, MX>(a, shmem, st);
 }
 
 // Rotated launches (Planes14): the LDS of a plain launch plus the f32
@@ -1544,17 +1628,29 @@ static int launch_gemv_rotated(const GemvArgs& a, hipStream_t st) {
 // Batch width of the next chunk of a batched launch: 2, 4, 8 or 16 (the next
 // power of two at or above the vectors left, at most 16; vectors past the
 // chunk's count read zero), narrowed until the activations fit in LDS; 1 for
-// a single vector left, or when not even two fit.
-static int batch_width(const GemvArgs& a, int left) {
-  if (left <= 1) return 1;
+// a single vector left on the dot-product path, or when not even two fit.  On
+// the matrix-core path a single vector left still runs 2 wide, so that every
+// vector of a batch gets the same arithmetic.
+static int batch_width(const GemvArgs& a, int left, bool mx) {
+  if (left <= 1 && !mx) return 1;
   for (int w = left > 8 ? 16 : left > 4 ? 8 : left > 2 ? 4 : 2; w >= 2; w >>= 1) {
     const size_t need = w == 16  ? gemv_lds_bytes<LEECH_PLANES14, 16>(a)
                         : w == 8 ? gemv_lds_bytes<LEECH_PLANES14, 8>(a)
                         : w == 4 ? gemv_lds_bytes<LEECH_PLANES14, 4>(a)
                                  : gemv_lds_bytes<LEECH_PLANES14, 2>(a);
-    if (need <= 160 * 1024) return w;
+    if (need + (mx ? 48 : 0) <= 160 * 1024) return w;     // mx: and the zero block
   }
   return 1;
+}
+
+// Products of batched launches: the matrix cores where the geometry allows
+// (tile_rows a multiple of 16), or v_dot2 per activation.
+static std::atomic<int> g_batch_mode{LEECH_BATCH_AUTO};
+
+template <int NB>
+static int launch_batch(const GemvArgs& c, bool mx, hipStream_t st) {
+  return mx ? launch_gemv<LEECH_PLANES14, NB, false, true>(c, st)
+            : launch_gemv<LEECH_PLANES14, NB>(c, st);
 }
 
 template <int LAYOUT>
@@ -1647,16 +1743,18 @@ int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const vo
   a.ldx = ldx;
   a.ldy = ldy;
   const hipStream_t st = (hipStream_t)stream;
+  const bool mx = batch > 1 && g_batch_mode.load(std::memory_order_relaxed) == LEECH_BATCH_AUTO &&
+                  a.R % 16 == 0;
   for (int b0 = 0; b0 < batch;) {
-    const int w = batch_width(a, batch - b0);
+    const int w = batch_width(a, batch - b0, mx);
     GemvArgs c = a;
     c.x = d_X + (int64_t)b0 * ldx;
     c.y = d_Y + (int64_t)b0 * ldy;
     c.nbatch = std::min(w, batch - b0);
-    rc = w == 16  ? launch_gemv<LEECH_PLANES14, 16>(c, st)
-         : w == 8 ? launch_gemv<LEECH_PLANES14, 8>(c, st)
-         : w == 4 ? launch_gemv<LEECH_PLANES14, 4>(c, st)
-         : w == 2 ? launch_gemv<LEECH_PLANES14, 2>(c, st)
+    rc = w == 16  ? launch_batch<16>(c, mx, st)
+         : w == 8 ? launch_batch<8>(c, mx, st)
+         : w == 4 ? launch_batch<4>(c, mx, st)
+         : w == 2 ? launch_batch<2>(c, mx, st)
                   : gemv_dispatch(desc, c, st);
     if (rc) return rc;
     b0 += c.nbatch;
@@ -1812,6 +1910,14 @@ int leech_set_exception_mode(int mode) {
   if (mode != LEECH_EXC_HOISTED && mode != LEECH_EXC_INLINE)
     return set_error(LEECH_E_ARG, "exception mode must be LEECH_EXC_HOISTED or LEECH_EXC_INLINE");
   g_exc_mode.store(mode, std::memory_order_relaxed);
+  return LEECH_OK;
+}
+
+int leech_set_batch_mode(int mode) {
+  clear_error();
+  if (mode != LEECH_BATCH_AUTO && mode != LEECH_BATCH_DOT2)
+    return set_error(LEECH_E_ARG, "batch mode must be LEECH_BATCH_AUTO or LEECH_BATCH_DOT2");
+  g_batch_mode.store(mode, std::memory_order_relaxed);
   return LEECH_OK;
 }
 

@@ -1,7 +1,12 @@
-"""Batched GEMV (Planes14) through the C ABI: every output vector is
-bit-identical to the single GEMV of its activation and within tolerance of
-the oracle's f64 product; batches not a power of two, batches above 8, wide K
-(narrower chunks), strided activations and outputs."""
+"""Batched GEMV (Planes14) through the C ABI.  With v_dot2 products
+(BATCH_DOT2, and geometries whose tile_rows is not a multiple of 16) every
+output vector is bit-identical to the single GEMV of its activation; with the
+matrix-core products (BATCH_AUTO where tile_rows is a multiple of 16) each
+vector is within tolerance of the oracle's f64 product and of its single
+GEMV, and bit-identical whatever the batch size and its position in the
+batch.  Batches not a power of two, above 16, wide K (narrower chunks), every
+geometry the matrix-core path takes (ragged tiles, lanes without a column),
+strided activations and outputs."""
 import sys
 
 import numpy as np
@@ -38,27 +43,137 @@ def activations(K, B, seed):
     return np.stack([synth.make_activation(K, seed=seed + b, name="batch") for b in range(B)])
 
 
-@pytest.mark.parametrize("M,K,B", [(1, 24, 2), (65, 408, 3), (257, 792, 8), (768, 1536, 5),
-                                   (4096, 4096, 11), (14337, 120, 4), (1024, 17408, 8),
-                                   (300, 24 * 30, 1), (768, 1536, 21), (257, 792, 16)])
-def test_batch_matches_single_and_oracle(dev, dcb, M, K, B):
-    say(f"[batch] {M}x{K} B={B}")
-    inp = synth.make_gemv_inputs(M, K, seed=M + B, name="batch")
+def oracle_check(inp, rows, X, Y, bs):
+    sub = synth.GemvInputs(len(rows), inp.K, inp.Kpad, inp.nb, inp.z[rows], inp.gain[rows],
+                           inp.scale[rows], inp.x, inp.seed, inp.name)
+    W = D.weights64_from_points(sub.z, sub.gain, sub.scale, CEN)
+    for b in bs:
+        e = D.errors(Y[b][rows], D.gemv64(W, X[b]), W, X[b])
+        assert e["max_norm_err"] <= 2e-3 and e["max_abs_err"] <= 1e-5, (b, e)
+    return W
+
+
+def sample_rows(M):
+    return np.arange(M) if M <= 1024 else np.sort(np.random.default_rng(M).choice(M, 256, False))
+
+
+def build(dev, dcb, M, K, seed, geometry=None):
+    inp = synth.make_gemv_inputs(M, K, seed=seed, name="batch")
     cls, sm, lv = dcb.cb.fields_from_points(inp.z)
-    mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+    mat = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev,
+                                    geometry=geometry)
+    return inp, mat
+
+
+def matrix_cores(mat, B):
+    return B > 1 and mat.desc.tile_rows % 16 == 0
+
+
+@pytest.fixture
+def dot2_mode():
+    P.set_batch_mode(P.BATCH_DOT2)
+    yield
+    P.set_batch_mode(P.BATCH_AUTO)
+
+
+SHAPES = [(1, 24, 2), (65, 408, 3), (257, 792, 8), (768, 1536, 5), (4096, 4096, 11),
+          (14337, 120, 4), (1024, 17408, 8), (300, 24 * 30, 1), (768, 1536, 21), (257, 792, 16)]
+
+
+@pytest.mark.parametrize("M,K,B", SHAPES)
+def test_dot2_batch_bit_identical_to_single(dev, dcb, dot2_mode, M, K, B):
+    say(f"[batch dot2] {M}x{K} B={B}")
+    inp, mat = build(dev, dcb, M, K, M + B)
     X = activations(K, B, seed=K)
     Xd = torch.from_numpy(X).to(dev)
     Y = mat.gemv_batch(Xd, centroids=CEN).cpu().numpy()
     for b in range(B):
         y1 = mat.gemv(Xd[b].contiguous(), centroids=CEN).cpu().numpy()
         assert np.array_equal(Y[b].view(np.uint32), y1.view(np.uint32)), f"vector {b}"
-    rows = np.arange(M) if M <= 1024 else np.sort(np.random.default_rng(M).choice(M, 256, False))
-    sub = synth.GemvInputs(len(rows), inp.K, inp.Kpad, inp.nb, inp.z[rows], inp.gain[rows],
-                           inp.scale[rows], inp.x, inp.seed, inp.name)
-    W = D.weights64_from_points(sub.z, sub.gain, sub.scale, CEN)
+    oracle_check(inp, sample_rows(M), X, Y, (0, B - 1))
+
+
+def check_auto(dev, mat, inp, X, Y):
+    """Y from BATCH_AUTO: bit-identical to single GEMVs where the products are
+    v_dot2; on the matrix cores within tolerance of the oracle and, row by
+    row, within 2^-15 · Σ|w x| of the single GEMV.  The bound: a block's
+    24-product dot of the decoded (subnormal) weights with an N(0,1) binary16
+    activation errs by at most 119 (v_dot2) and 155 (matrix core) units of
+    2^-24 · Σ|h x| over 512,000 measured dot products, so two paths differ by
+    under 2^-15 · Σ|h x| a block; the blocks' f32 accumulation adds a few
+    more units."""
+    B = X.shape[0]
+    Xd = torch.from_numpy(X).to(dev)
+    rows = sample_rows(inp.M)
+    if not matrix_cores(mat, B):
+        for b in range(B):
+            y1 = mat.gemv(Xd[b].contiguous(), centroids=CEN).cpu().numpy()
+            assert np.array_equal(Y[b].view(np.uint32), y1.view(np.uint32)), f"vector {b}"
+        oracle_check(inp, rows, X, Y, (0, B - 1))
+        return
+    W = oracle_check(inp, rows, X, Y, range(B))
     for b in (0, B - 1):
-        e = D.errors(Y[b][rows], D.gemv64(W, X[b]), W, X[b])
-        assert e["max_norm_err"] <= 2e-3 and e["max_abs_err"] <= 1e-5, (b, e)
+        y1 = mat.gemv(Xd[b].contiguous(), centroids=CEN).cpu().numpy()
+        bound = 2.0 ** -15 * (np.abs(W) @ np.abs(X[b].astype(np.float64)))
+        diff = np.abs(Y[b][rows].astype(np.float64) - y1[rows])
+        assert (diff <= bound).all(), (b, float((diff / np.maximum(bound, 1e-300)).max()))
+
+
+@pytest.mark.parametrize("M,K,B", SHAPES)
+def test_batch_matches_oracle_and_single(dev, dcb, M, K, B):
+    say(f"[batch] {M}x{K} B={B}")
+    inp, mat = build(dev, dcb, M, K, M + B)
+    say(f"[batch] geometry {mat.desc.lane_cols}x{mat.desc.tile_rows}, "
+        f"matrix cores {matrix_cores(mat, B)}")
+    X = activations(K, B, seed=K)
+    Y = mat.gemv_batch(torch.from_numpy(X).to(dev), centroids=CEN).cpu().numpy()
+    check_auto(dev, mat, inp, X, Y)
+
+
+# every placement the matrix-core path takes: one column per group of lanes
+# (C = 1, R = 16..64), two and four columns, three columns with a lane group
+# past the last column (C = 3, R = 16), and R · C < 64; ragged last tiles and
+# last column groups
+MX_GEOMETRIES = [((1, 64), 1000, 24 * 37), ((2, 32), 777, 24 * 41), ((4, 16), 301, 24 * 43),
+                 ((3, 16), 333, 24 * 29), ((1, 16), 70, 24 * 11), ((1, 48), 100, 24 * 7),
+                 ((2, 16), 50, 24 * 9), ((1, 32), 33, 24), ((4, 16), 4096, 4104)]
+
+
+@pytest.mark.parametrize("geo,M,K", MX_GEOMETRIES)
+def test_matrix_core_geometries(dev, dcb, geo, M, K):
+    inp, mat = build(dev, dcb, M, K, M + K, geometry=geo)
+    assert (mat.desc.lane_cols, mat.desc.tile_rows) == geo
+    for B in (2, 3, 5, 16, 17):
+        say(f"[batch mx] {geo} {M}x{K} B={B}")
+        X = activations(K, B, seed=K + B)
+        Y = mat.gemv_batch(torch.from_numpy(X).to(dev), centroids=CEN).cpu().numpy()
+        check_auto(dev, mat, inp, X, Y)
+
+
+@pytest.mark.parametrize("geo,M,K", [((4, 16), 301, 24 * 43), ((2, 32), 777, 24 * 41),
+                                     ((1, 64), 1000, 24 * 37)])
+def test_matrix_core_bits_independent_of_batch(dev, dcb, geo, M, K):
+    """One activation's y is the same bits alone in a 2-wide launch, in
+    every position of 4-, 8- and 16-wide launches and in a trailing chunk."""
+    inp, mat = build(dev, dcb, M, K, 3 * M + K, geometry=geo)
+    X = activations(K, 17, seed=K)
+    Xd = torch.from_numpy(X).to(dev)
+    ref = mat.gemv_batch(Xd[:2], centroids=CEN).cpu().numpy()
+    for B in (3, 4, 8, 16, 17):
+        say(f"[batch bits] {geo} B={B}")
+        Y = mat.gemv_batch(Xd[:B], centroids=CEN).cpu().numpy()
+        assert np.array_equal(Y[:2].view(np.uint32), ref.view(np.uint32)), B
+    full = mat.gemv_batch(Xd, centroids=CEN).cpu().numpy()
+    for shift in (1, 5, 13, 16):
+        say(f"[batch bits] {geo} shift {shift}")
+        Y = mat.gemv_batch(torch.roll(Xd, shift, 0).contiguous(), centroids=CEN).cpu().numpy()
+        assert np.array_equal(Y.view(np.uint32), np.roll(full, shift, 0).view(np.uint32)), shift
+
+
+def test_batch_mode_rejects_unknown(dev):
+    with pytest.raises(P.LeechError):
+        P.set_batch_mode(7)
+    P.set_batch_mode(P.BATCH_AUTO)
 
 
 def test_strided_activations_and_outputs(dev, dcb):

@@ -369,3 +369,16 @@ def test_paper_byte_accounting(cb):
         assert abs(rate[k] - v) < 0.0015, (k, rate[k])
     gb = {"fp16": 2 * params, "planes14": 14 * blocks + tail}
     assert round(gb["fp16"] / 1e9, 2) == 7.27 and round(gb["planes14"] / 1e9, 2) == 2.18
+
+
+def test_mode_setters_reject_unknown_values():
+    """The process-wide mode setters are host code: unknown values fail with
+    LEECH_E_ARG and leave the mode as it was."""
+    with pytest.raises(P.LeechError):
+        P.set_batch_mode(2)
+    with pytest.raises(P.LeechError):
+        P.set_prologue_mode(3)
+    with pytest.raises(P.LeechError):
+        P.set_exception_mode(5)
+    P.set_batch_mode(P.BATCH_DOT2)
+    P.set_batch_mode(P.BATCH_AUTO)
