@@ -964,18 +964,39 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   // then the pipeline's record loads, then the LDS writes, which wait only for
   // the older staging loads.
   constexpr int kXPer = XPER;                  // x blocks per thread held in registers
+  constexpr int kXChunk = 4;                   // batched: x blocks per thread per round trip
   constexpr int kEPer = kExcPrefetch, kUPer = 2;
   // rare overflow first (xblocks > kXPer·threads, or fewer threads than
   // classes): loads of unknown count here, before the ordered ones.  Only the
   // ball's class ids occur in a layout, so only their entries are staged, both
   // gain entries of a class from one read of its table record.
-  // (a batched launch stages all its activations here: vector b's blocks
-  // follow vector b − 1's, zero past nb and for vectors past nbatch)
-  if constexpr (!ROT)
-  for (int j = NB == 1 ? tid + kXPer * nthr : tid; j < NB * xblocks + (MX ? 1 : 0); j += nthr) {
-    const int b = NB == 1 ? 0 : j / xblocks, jb = j - b * xblocks;
-    if (jb < nb && b < a.nbatch) {
-      store_x_block(load_x_block(a.x + b * a.ldx + 24 * (int64_t)jb), xs + 12 * j);
+  if constexpr (NB > 1) {
+    // A batched launch stages all its activations here, kXChunk blocks a
+    // thread in flight at a time: vector b's blocks follow vector b − 1's,
+    // zero past nb and for vectors past nbatch (MX: and the zero block after
+    // them).  (Requested after the first records instead, they return behind
+    // them: loads return in order, and the launch is slower.)
+    const int total = NB * xblocks + (MX ? 1 : 0);
+    for (int j0 = tid; j0 < total; j0 += kXChunk * nthr) {
+      XBlock r[kXChunk];
+#pragma unroll
+      for (int u = 0; u < kXChunk; ++u) {
+        const int j = j0 + u * nthr;
+        const int b = j / xblocks, jb = j - b * xblocks;
+        if (j < total && jb < nb && b < a.nbatch)
+          r[u] = load_x_block(a.x + b * a.ldx + 24 * (int64_t)jb);
+        else
+          r[u].v0 = r[u].v1 = r[u].v2 = u32x4a{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int u = 0; u < kXChunk; ++u)
+        if (j0 + u * nthr < total) store_x_block(r[u], xs + 12 * (j0 + u * nthr));
+    }
+  }
+  if constexpr (NB == 1 && !ROT)
+  for (int j = tid + kXPer * nthr; j < xblocks; j += nthr) {
+    if (j < nb) {
+      store_x_block(load_x_block(a.x + 24 * (int64_t)j), xs + 12 * j);
     } else {
       u32x4a* d = (u32x4a*)(xs + 12 * j);
       d[0] = d[1] = d[2] = u32x4a{0, 0, 0, 0};
