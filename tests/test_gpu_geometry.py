@@ -7,8 +7,9 @@ that share a tile, through the C ABI.
   each layout decodes bit-exactly to the drawn points, all four layouts (and
   both exception decoders) give bit-identical y, and y is within the GEMV
   tolerance of the oracle's f64 matvec on every row.
-* The batched and rotated entry points on a three-column geometry give the
-  single GEMV's and the two-call bits.
+* The batched and rotated entry points on geometries whose tile_rows is not
+  a multiple of 16 (v_dot2 batches) give the single GEMV's and the two-call
+  bits.
 * Row groups whose boundaries fall inside tiles (each such tile holds rows of
   two groups, every lane reading its own row's centroids): every row matches
   the oracle with its own group's centroids, in every layout, bit-identical

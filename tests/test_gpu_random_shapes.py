@@ -4,7 +4,9 @@ column group's width take many combinations the fixed cases do not.  For each
 shape every layout must decode bit-exactly to the drawn points, all four
 layouts must give bit-identical y, y must be within the GEMV tolerance of the
 oracle on sampled rows, and, on a third of the shapes, the batched, grouped
-and rotated entry points must give the single GEMV's or the two-call bits.
+and rotated entry points must give the single GEMV's or the two-call bits
+(batches on the matrix cores: within the dot units' rounding of the single
+GEMV, and its bits in the v_dot2 mode).
 """
 import sys
 
@@ -75,7 +77,18 @@ def test_random_shape(dev, dcb, i):
     # batched: three activations, the first being x
     X = np.stack([inp.x] + [synth.make_activation(K, seed=1000 + i + b, name="random-shape")
                             for b in range(2)])
-    Y = p14.gemv_batch(torch.from_numpy(X).to(dev), centroids=CEN).cpu().numpy()
+    Xd = torch.from_numpy(X).to(dev)
+    Y = p14.gemv_batch(Xd, centroids=CEN).cpu().numpy()
+    if p14.desc.tile_rows % 16 == 0:
+        # matrix-core products: within 2^-15 · Σ|w x| of the single GEMV (the
+        # dot units' measured rounding), and the v_dot2 mode gives its bits
+        bound = 2.0 ** -15 * (np.abs(W) @ np.abs(inp.x.astype(np.float64)))
+        assert (np.abs(Y[0][rows].astype(np.float64) - y1[rows]) <= bound).all()
+        P.set_batch_mode(P.BATCH_DOT2)
+        try:
+            Y = p14.gemv_batch(Xd, centroids=CEN).cpu().numpy()
+        finally:
+            P.set_batch_mode(P.BATCH_AUTO)
     assert np.array_equal(Y[0].view(np.uint32), y1.view(np.uint32))
     # grouped, one group: the plain call's bits
     yg = p14.gemv_grouped(x, [M], [CEN]).cpu().numpy()
