@@ -916,9 +916,9 @@ def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
     """Batched GEMV (§6 "Batching") on the bench workload in Planes14: µs per
     launch of Y = W X for B activations (each block decoded once for up to 16
     of them), walking the same replicas as the Planes14 arm, with the
-    library's default products (matrix cores where tile_rows is a multiple of
-    16) and, for B > 1, with v_dot2 per activation (dot2_us); the largest
-    normalised difference of Y[0] and Y[B-1] from their single GEMVs; beside
+    library's default products (matrix cores where the geometry allows) and,
+    for B > 1, with v_dot2 per activation (dot2_us); the largest normalised
+    difference of Y[0] and Y[B-1] from their single GEMVs; beside
     it the FP16 weights through the library GEMM (torch.matmul, hipBLASLt) on
     the same B, as the batched FP16 reference."""
     import numpy as np
@@ -938,7 +938,7 @@ def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
             y1 = leech[0].gemv(X[b].contiguous())
             diff = max(diff, float((Y[b] - y1).abs().max() / y1.abs().max()))
         us = replay_us(torch, lambda i: leech[i % reps].gemv_batch(X, Y), args.layer_steps)
-        mx = B > 1 and leech[0].desc.tile_rows % 16 == 0
+        mx = B > 1 and leech[0].batch_on_matrix_cores
         row = {"us": round(us, 2), "us_per_vector": round(us / B, 3),
                "weight_GBps": round(p14.served_bytes / (us * 1e-6) / 1e9, 1),
                "products": "mfma" if mx else "dot2", "max_norm_diff_vs_single": diff}

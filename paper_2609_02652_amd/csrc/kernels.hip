@@ -857,10 +857,11 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // NB: batch width (1, 2, 4, 8 or 16).  Each decoded block is multiplied with
 // NB activations (NB > 1: Planes14), in the same order as a single GEMV, so
 // every output vector is bit-identical to that activation's own GEMV.
-// MX (NB > 1, tile_rows a multiple of 16): the products go through the matrix
-// cores instead.  Lanes are placed by column (lane c·R + r holds block (r, c)
-// of the unit, R = tile_rows), so each 16-lane group of a wave holds blocks of
-// one block column.  The decoded block is the B operand (column l % 16, its
+// MX (NB > 1, lane_cols · 16·ceil(tile_rows / 16) ≤ 64): the products go
+// through the matrix cores instead.  Lanes are placed by column (lane c·Rp + r
+// holds block (r, c) of the unit, Rp = tile_rows rounded up to a multiple of
+// 16; lanes r ≥ tile_rows hold stand-ins), so each 16-lane group of a wave
+// holds blocks of one block column.  The decoded block is the B operand (column l % 16, its
 // 24 values over three 16×16×32 products); A is block-diagonal: row 4q + i
 // carries activation i's 8 values of group q's column in group q's k range and
 // zeros elsewhere.  D row 4q + i, column n is then the dot product of lane
@@ -922,7 +923,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   };
   if (wave == 0) stamp(0);
-  const int rl = MX ? lane % a.R : lane / C, cl = MX ? lane / a.R : lane % C;
+  // MX: lanes by column, each column's lanes padded to a multiple of 16
+  const int Rp = (a.R + 15) & ~15;
+  const int rl = MX ? lane % Rp : lane / C, cl = MX ? lane / Rp : lane % C;
   const int gf = groups - 1;                      // full-width column groups
   const int C_last = (int)(nb - (int64_t)gf * C);
   const bool row_ok = rl < R_t && (!MX || cl < C), last_ok = row_ok && cl < C_last;
@@ -1383,7 +1386,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const float v = MX ? row_sum_cols(acc[b], C, a.R) : row_sum(acc[b], C);
+    const float v = MX ? row_sum_cols(acc[b], C, Rp) : row_sum(acc[b], C);
     if (cl == 0 && rl < R_t) red[(b * waves + wave) * 64 + rl] = v;
   }
   __syncthreads();
@@ -1664,8 +1667,11 @@ static int batch_width(const GemvArgs& a, int left, bool mx) {
   return 1;
 }
 
-// Products of batched launches: the matrix cores where the geometry allows
-// (tile_rows a multiple of 16), or v_dot2 per activation.
+// Products of batched launches: the matrix cores where the geometry allows, or
+// v_dot2 per activation.  The matrix-core form places lanes by column, each
+// column's lanes padded to a multiple of 16 (one block column per
+// quarter-wave), so it needs lane_cols · 16·ceil(tile_rows / 16) ≤ 64.
+static bool batch_on_matrix_cores(int C, int R) { return C * ((R + 15) / 16 * 16) <= 64; }
 static std::atomic<int> g_batch_mode{LEECH_BATCH_AUTO};
 
 template <int NB>
@@ -1765,7 +1771,7 @@ int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const vo
   a.ldy = ldy;
   const hipStream_t st = (hipStream_t)stream;
   const bool mx = batch > 1 && g_batch_mode.load(std::memory_order_relaxed) == LEECH_BATCH_AUTO &&
-                  a.R % 16 == 0;
+                  batch_on_matrix_cores(a.C, a.R);
   for (int b0 = 0; b0 < batch;) {
     const int w = batch_width(a, batch - b0, mx);
     GemvArgs c = a;

@@ -180,10 +180,10 @@ def test_every_class_batched_grouped_rotated(dev, dcb, M, nb, sort_by_class):
         Yd = mat.gemv_batch(Xd, centroids=CEN).cpu().numpy()
     finally:
         P.set_batch_mode(P.BATCH_AUTO)
-    # matrix-core products where tile_rows is a multiple of 16: within
+    # matrix-core products where the geometry takes them: within
     # 2^-15 · Σ|w x| of the single GEMV (the dot units' measured rounding);
     # v_dot2 products: the single GEMV's bits
-    mx = mat.desc.tile_rows % 16 == 0
+    mx = mat.batch_on_matrix_cores
     for b in range(3):
         yb = mat.gemv(Xd[b].contiguous(), centroids=CEN).cpu().numpy()
         assert np.array_equal(Yd[b].view(np.uint32), yb.view(np.uint32)), b

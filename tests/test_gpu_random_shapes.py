@@ -79,7 +79,7 @@ def test_random_shape(dev, dcb, i):
                             for b in range(2)])
     Xd = torch.from_numpy(X).to(dev)
     Y = p14.gemv_batch(Xd, centroids=CEN).cpu().numpy()
-    if p14.desc.tile_rows % 16 == 0:
+    if p14.batch_on_matrix_cores:
         # matrix-core products: within 2^-15 · Σ|w x| of the single GEMV (the
         # dot units' measured rounding), and the v_dot2 mode gives its bits
         bound = 2.0 ** -15 * (np.abs(W) @ np.abs(inp.x.astype(np.float64)))
