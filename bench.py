@@ -93,6 +93,8 @@ def parse():
     ap.add_argument("--no-step14b", action="store_true",
                     help="skip the 14B-class decode step (40 layers + fp16 head, Leech vs FP16)")
     ap.add_argument("--step14b-layers", type=int, default=40)
+    ap.add_argument("--batch-14b", action="store_true",
+                    help="also time batched launches at the 14B-class fused projection shapes")
     ap.add_argument("--sweep", action="store_true",
                     help="also time square Planes14 GEMVs from 1024x1024 to 16384x16384")
     ap.add_argument("--no-large", action="store_true",
@@ -974,6 +976,59 @@ def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
     return res
 
 
+BATCH_14B = [("q/k/v fused", 7168, 5136), ("o", 5120, 5136), ("gate/up fused", 34816, 5136),
+             ("down", 5120, 17424)]
+
+
+def bench_batch_14b(args, torch, P, synth, batches=(4, 16)):
+    """Batched launches (§6 "Batching") at the 14B-class fused projection
+    shapes, Planes14 in the library's geometry and, for the 3 x 20 shapes
+    (whose batches the matrix-core form cannot take), also expanded in the
+    4 x 16 geometry: µs per launch of Y = W X for B activations with the
+    default products and with v_dot2, graph replay of args.layer_steps
+    launches over replicas of >= 1 GiB."""
+    import numpy as np
+    dev = torch.device("cuda:0")
+    dcb = P.DeviceCodebook(P.Codebook(12), dev)
+    res = {}
+    for i, (name, M, K) in enumerate(BATCH_14B):
+        inp = synth.make_gemv_inputs(M, K, seed=2000 + i, name=f"batch14b-{name}")
+        cls, sm, lv = dcb.cb.fields_from_points(inp.z)
+        prev = None
+        for geo in (None, (4, 16)):
+            # the 4 x 16 expansion only where the library's geometry keeps
+            # batches off the matrix cores
+            if prev is not None and prev["matrix_cores"]:
+                break
+            m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev,
+                                           geometry=geo)
+            reps = max(1, math.ceil(REPLICA_BYTES / m0.desc.served_bytes))
+            mats = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0.clone(),
+                                         m0.side1.clone(), m0.scale.clone(), dcb)
+                           for _ in range(reps - 1)]
+            row = {"geometry": f"{m0.desc.lane_cols}x{m0.desc.tile_rows}",
+                   "matrix_cores": m0.batch_on_matrix_cores, "replicas": reps}
+            for B in batches:
+                X = torch.from_numpy(np.stack([synth.make_activation(K, seed=60 + b, name="batch14b")
+                                               for b in range(B)])).to(dev)
+                Y = torch.empty((B, M), dtype=torch.float32, device=dev)
+                row[f"B{B}_us"] = round(replay_us(torch, lambda j: mats[j % reps].gemv_batch(X, Y),
+                                                  args.layer_steps), 2)
+                P.set_batch_mode(P.BATCH_DOT2)
+                try:
+                    row[f"B{B}_dot2_us"] = round(replay_us(
+                        torch, lambda j: mats[j % reps].gemv_batch(X, Y), args.layer_steps), 2)
+                finally:
+                    P.set_batch_mode(P.BATCH_AUTO)
+            key = f"{name} {M}x{K}" + ("" if geo is None else " (4x16 expansion)")
+            res[key] = row
+            prev = row
+            log(f"[bench] batch 14B {key}: {row}")
+            del mats, m0
+            torch.cuda.empty_cache()
+    return res
+
+
 def bench_rotation(args, torch, P, synth, widths=(4096, 14336, 17408)):
     """µs per activation rotation (blockwise Walsh–Hadamard, fp16 in and out)
     at the 8B and 14B site widths: one graph replay of args.layer_steps
@@ -1479,6 +1534,13 @@ def main():
         torch.cuda.synchronize()
         large = bench_large(args, torch, P, synth)
 
+    batch14b = None
+    if args.batch_14b:
+        for a in arms.values():
+            a._graphs.clear()
+        torch.cuda.synchronize()
+        batch14b = bench_batch_14b(args, torch, P, synth)
+
     sweep = None
     if args.sweep:
         for a in arms.values():
@@ -1537,6 +1599,7 @@ def main():
         "layer_8b": layer,
         "step_14b": step14b,
         "large": large,
+        "batch_14b": batch14b,
         "sweep": sweep,
         "launch_floor": floor,
         "cpu_baseline": cpu,
