@@ -918,8 +918,8 @@ def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
     """Batched GEMV (§6 "Batching") on the bench workload in Planes14: µs per
     launch of Y = W X for B activations (each block decoded once for up to 16
     of them), walking the same replicas as the Planes14 arm, with the
-    library's default products (matrix cores where the geometry allows) and,
-    for B > 1, with v_dot2 per activation (dot2_us); the largest normalised
+    library's default products (the matrix cores for B > 1) and, for B > 1,
+    with v_dot2 per activation (dot2_us); the largest normalised
     difference of Y[0] and Y[B-1] from their single GEMVs; beside
     it the FP16 weights through the library GEMM (torch.matmul, hipBLASLt) on
     the same B, as the batched FP16 reference."""
@@ -940,7 +940,7 @@ def bench_batch(args, torch, P, synth, inp, arms, batches=(1, 2, 4, 8, 16)):
             y1 = leech[0].gemv(X[b].contiguous())
             diff = max(diff, float((Y[b] - y1).abs().max() / y1.abs().max()))
         us = replay_us(torch, lambda i: leech[i % reps].gemv_batch(X, Y), args.layer_steps)
-        mx = B > 1 and leech[0].batch_on_matrix_cores
+        mx = B > 1
         row = {"us": round(us, 2), "us_per_vector": round(us / B, 3),
                "weight_GBps": round(p14.served_bytes / (us * 1e-6) / 1e9, 1),
                "products": "mfma" if mx else "dot2", "max_norm_diff_vs_single": diff}
@@ -982,11 +982,9 @@ BATCH_14B = [("q/k/v fused", 7168, 5136), ("o", 5120, 5136), ("gate/up fused", 3
 
 def bench_batch_14b(args, torch, P, synth, batches=(4, 16)):
     """Batched launches (§6 "Batching") at the 14B-class fused projection
-    shapes, Planes14 in the library's geometry and, for the 3 x 20 shapes
-    (whose batches the matrix-core form cannot take), also expanded in the
-    4 x 16 geometry: µs per launch of Y = W X for B activations with the
-    default products and with v_dot2, graph replay of args.layer_steps
-    launches over replicas of >= 1 GiB."""
+    shapes, Planes14 in the library's geometry: µs per launch of Y = W X for B
+    activations on the matrix cores (the default) and with v_dot2, graph
+    replay of args.layer_steps launches over replicas of >= 1 GiB."""
     import numpy as np
     dev = torch.device("cuda:0")
     dcb = P.DeviceCodebook(P.Codebook(12), dev)
@@ -994,38 +992,29 @@ def bench_batch_14b(args, torch, P, synth, batches=(4, 16)):
     for i, (name, M, K) in enumerate(BATCH_14B):
         inp = synth.make_gemv_inputs(M, K, seed=2000 + i, name=f"batch14b-{name}")
         cls, sm, lv = dcb.cb.fields_from_points(inp.z)
-        prev = None
-        for geo in (None, (4, 16)):
-            # the 4 x 16 expansion only where the library's geometry keeps
-            # batches off the matrix cores
-            if prev is not None and prev["matrix_cores"]:
-                break
-            m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev,
-                                           geometry=geo)
-            reps = max(1, math.ceil(REPLICA_BYTES / m0.desc.served_bytes))
-            mats = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0.clone(),
-                                         m0.side1.clone(), m0.scale.clone(), dcb)
-                           for _ in range(reps - 1)]
-            row = {"geometry": f"{m0.desc.lane_cols}x{m0.desc.tile_rows}",
-                   "matrix_cores": m0.batch_on_matrix_cores, "replicas": reps}
-            for B in batches:
-                X = torch.from_numpy(np.stack([synth.make_activation(K, seed=60 + b, name="batch14b")
-                                               for b in range(B)])).to(dev)
-                Y = torch.empty((B, M), dtype=torch.float32, device=dev)
-                row[f"B{B}_us"] = round(replay_us(torch, lambda j: mats[j % reps].gemv_batch(X, Y),
-                                                  args.layer_steps), 2)
-                P.set_batch_mode(P.BATCH_DOT2)
-                try:
-                    row[f"B{B}_dot2_us"] = round(replay_us(
-                        torch, lambda j: mats[j % reps].gemv_batch(X, Y), args.layer_steps), 2)
-                finally:
-                    P.set_batch_mode(P.BATCH_AUTO)
-            key = f"{name} {M}x{K}" + ("" if geo is None else " (4x16 expansion)")
-            res[key] = row
-            prev = row
-            log(f"[bench] batch 14B {key}: {row}")
-            del mats, m0
-            torch.cuda.empty_cache()
+        m0 = P.LeechMatrix.from_fields(dcb, P.PLANES14, cls, inp.gain, sm, lv, inp.scale, dev)
+        reps = max(1, math.ceil(REPLICA_BYTES / m0.desc.served_bytes))
+        mats = [m0] + [P.LeechMatrix(m0.desc, m0.main.clone(), m0.side0.clone(),
+                                     m0.side1.clone(), m0.scale.clone(), dcb)
+                       for _ in range(reps - 1)]
+        row = {"geometry": f"{m0.desc.lane_cols}x{m0.desc.tile_rows}", "replicas": reps}
+        for B in batches:
+            X = torch.from_numpy(np.stack([synth.make_activation(K, seed=60 + b, name="batch14b")
+                                           for b in range(B)])).to(dev)
+            Y = torch.empty((B, M), dtype=torch.float32, device=dev)
+            row[f"B{B}_us"] = round(replay_us(torch, lambda j: mats[j % reps].gemv_batch(X, Y),
+                                              args.layer_steps), 2)
+            P.set_batch_mode(P.BATCH_DOT2)
+            try:
+                row[f"B{B}_dot2_us"] = round(replay_us(
+                    torch, lambda j: mats[j % reps].gemv_batch(X, Y), args.layer_steps), 2)
+            finally:
+                P.set_batch_mode(P.BATCH_AUTO)
+        key = f"{name} {M}x{K}"
+        res[key] = row
+        log(f"[bench] batch 14B {key}: {row}")
+        del mats, m0
+        torch.cuda.empty_cache()
     return res
 
 

@@ -310,8 +310,8 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
  * batches run in chunks of 16 (fewer where Kpad leaves too little LDS: 16
  * activations fit up to about Kpad = 4,600, 8 up to about 9,200, the exact
  * bound depending on the column groups' rounding).  Products as
- * leech_set_batch_mode selects: on the matrix cores (the default where the
- * geometry allows) Y[b] is within rounding of leech_gemv on X[b]
+ * leech_set_batch_mode selects: on the matrix cores (the default) Y[b] is
+ * within rounding of leech_gemv on X[b]
  * and a single vector left after the 16-wide chunks still runs 2 wide; with
  * v_dot2 Y[b] is bit-identical to leech_gemv on X[b].  batch > 1 serves
  * LEECH_PLANES14 (LEECH_E_LAYOUT otherwise) and needs ldx ≥ Kpad, ldx a
@@ -355,16 +355,14 @@ enum { LEECH_EXC_HOISTED = 0, LEECH_EXC_INLINE = 1 };
 int leech_set_exception_mode(int mode);
 
 /* Products of leech_gemv_batch calls with batch > 1 enqueued from this call on
- * (process-wide; §6 "Batching").  LEECH_BATCH_AUTO (default): where
- * lane_cols · 16·ceil(tile_rows / 16) ≤ 64 (every lane_cols = 1 geometry,
- * lane_cols 2 up to 32 rows, 3 and 4 up to 16), each decoded block meets its
- * activations on the matrix cores (16×16×32 binary16 products with f32 accumulation, one block's 24
- * products per output, so the block's scale and class factor still multiply
- * its f32 dot product); Y[b] is then within rounding of leech_gemv on X[b]
- * (the matrix core sums a block's products in its own order) and
- * bit-identical for a given X[b] whatever the batch size or X[b]'s position.
- * Other geometries, and LEECH_BATCH_DOT2: v_dot2 per activation, Y[b]
- * bit-identical to leech_gemv on X[b].  LEECH_E_ARG for another value. */
+ * (process-wide; §6 "Batching").  LEECH_BATCH_AUTO (default): each decoded
+ * block meets its activations on the matrix cores (16-block 4×4×4 binary16
+ * products with f32 accumulation, one block's 24 products per output, so the
+ * block's scale and class factor still multiply its f32 dot product); Y[b] is
+ * then within rounding of leech_gemv on X[b] (the matrix core sums a block's
+ * products in its own order) and bit-identical for a given X[b] whatever the
+ * batch size or X[b]'s position.  LEECH_BATCH_DOT2: v_dot2 per activation,
+ * Y[b] bit-identical to leech_gemv on X[b].  LEECH_E_ARG for another value. */
 enum { LEECH_BATCH_AUTO = 0, LEECH_BATCH_DOT2 = 1 };
 int leech_set_batch_mode(int mode);
 

@@ -142,13 +142,6 @@ class LeechMatrix:
                          x.data_ptr(), y.data_ptr(), stamps.data_ptr(), _stream(stream))
         return y
 
-    @property
-    def batch_on_matrix_cores(self):
-        """Whether batched launches of this matrix take the matrix-core
-        products under BATCH_AUTO: the library's rule, lane_cols ·
-        16·ceil(tile_rows / 16) ≤ 64."""
-        return self.desc.lane_cols * (-(-self.desc.tile_rows // 16) * 16) <= 64
-
     def gemv_batch(self, X, Y=None, centroids=(1.0, 1.0), stream=None):
         """Y[b] = W X[b]: X fp16 [B, Kpad] device tensor (row stride a multiple
         of 8), Y f32 [B, M]; each block decoded once for up to 16 activations,

@@ -352,8 +352,8 @@ BATCH_AUTO, BATCH_DOT2 = 0, 1
 
 def set_batch_mode(mode: int) -> None:
     """Process-wide: the products of batched GEMVs enqueued afterwards
-    (BATCH_AUTO: matrix cores where lane_cols * 16*ceil(tile_rows/16) <= 64;
-    BATCH_DOT2: v_dot2, bit-identical to single GEMVs)."""
+    (BATCH_AUTO: the matrix cores, 16-block 4x4x4 MFMAs; BATCH_DOT2: v_dot2,
+    bit-identical to single GEMVs)."""
     check(lib.leech_set_batch_mode(mode))
 
 

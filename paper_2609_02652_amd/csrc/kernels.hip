@@ -636,16 +636,23 @@ __device__ __forceinline__ float row_sum(float v, int C) {
   return v;
 }
 
-// Row sum of the column-placed lanes of a matrix-core launch: row r's C ≤ 4
-// lanes are r, r + R, r + 2R, r + 3R, fetched by ds_bpermute; lane r (c = 0)
-// gets v0 (C = 1), v0 + v1, (v0 + v1) + v2 or (v0 + v1) + (v2 + v3).  Every
-// lane is active here.
+// Row sum of the column-placed lanes of a matrix-core launch: row r's lanes
+// are r + c·R, fetched by ds_bpermute.  For C ≤ 4 lane r (c = 0) gets v0
+// (C = 1), v0 + v1, (v0 + v1) + v2 or (v0 + v1) + (v2 + v3); for C = 8 and 16
+// (R = 4 or 8, both powers of two) an xor butterfly over the column bits,
+// partners R, 2R, 4R, ... apart.  Every lane is active here.
 __device__ __forceinline__ float row_sum_cols(float v, int C, int R) {
   const int l = (int)(threadIdx.x & 63u);
   auto at = [&](int c) {
     return __builtin_bit_cast(
         float, __builtin_amdgcn_ds_bpermute(((l + c * R) & 63) << 2, __builtin_bit_cast(int, v)));
   };
+  if (C >= 8) {
+    for (int step = R; step < C * R; step <<= 1)
+      v += __builtin_bit_cast(
+          float, __builtin_amdgcn_ds_bpermute(((l ^ step) & 63) << 2, __builtin_bit_cast(int, v)));
+    return v;
+  }
   if (C == 1) return v;
   const float s01 = v + at(1);
   if (C == 2) return s01;
@@ -653,14 +660,15 @@ __device__ __forceinline__ float row_sum_cols(float v, int C, int R) {
   return s01 + (at(2) + at(3));
 }
 
-// One 16×16×32 binary16 matrix-core product (f32 accumulate) on operands held
-// as four pair words a lane: lane l holds k = 8·(l / 16) .. + 7 of row l % 16
-// of A and of column l % 16 of B; D row 4·(l / 16) + i, column l % 16 comes
-// back in d[i].
-typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
-__device__ __forceinline__ f32x4a mfma16(u32x4a a, u32x4a b, f32x4a d) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, a),
-                                                __builtin_bit_cast(half8_t, b), d, 0, 0, 0);
+// Sixteen 4×4×4 binary16 products at once (f32 accumulate): block q = l / 4;
+// lane 4q + i holds row i of A_q and column i of B_q (k = 0..3, two pair
+// words each); d[i] of lane 4q + j is D_q row i, column j.
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4a mfma4(uint32_t a0, uint32_t a1, uint32_t b0, uint32_t b1,
+                                        f32x4a d) {
+  return __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(half4_t, u32x2a{a0, a1}),
+                                            __builtin_bit_cast(half4_t, u32x2a{b0, b1}), d, 0, 0,
+                                            0);
 }
 
 // ------------------------------------------------------- fused rotation
@@ -857,22 +865,22 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // NB: batch width (1, 2, 4, 8 or 16).  Each decoded block is multiplied with
 // NB activations (NB > 1: Planes14), in the same order as a single GEMV, so
 // every output vector is bit-identical to that activation's own GEMV.
-// MX (NB > 1, lane_cols · 16·ceil(tile_rows / 16) ≤ 64): the products go
-// through the matrix cores instead.  Lanes are placed by column (lane c·Rp + r
-// holds block (r, c) of the unit, Rp = tile_rows rounded up to a multiple of
-// 16; lanes r ≥ tile_rows hold stand-ins), so each 16-lane group of a wave
-// holds blocks of one block column.  The decoded block is the B operand (column l % 16, its
-// 24 values over three 16×16×32 products); A is block-diagonal: row 4q + i
-// carries activation i's 8 values of group q's column in group q's k range and
-// zeros elsewhere.  D row 4q + i, column n is then the dot product of lane
-// 16q + n's own block with activation i, back in that lane's d[i]: four
-// activations per three products, no sum across blocks, so the block's scale
-// and class factor still multiply its f32 dot product.  The matrix core sums
-// the 24 products in its own order: outputs are within rounding of the
-// single GEMV's and bit-identical across batch widths (activation b always
-// sits in row b mod 4 of product set b / 4).  A lane of group q that carries
-// no activation (row group other than q, or an activation past NB) reads a
-// zero block staged after the activations.
+// MX (NB > 1): the products go through the matrix cores instead, as the
+// 16-block 4×4×4 binary16 MFMA with f32 accumulation.  Lanes are placed by
+// column (lane c·R + r holds block (r, c) of the unit, R = tile_rows, a
+// multiple of 4), so each block of 4 lanes holds blocks of one column.  In
+// block q = lane / 4, lane 4q + i supplies activation 4s + i's four values of
+// the column as A row i and four values of its own decoded block as B column
+// i; D row i, column j (lane 4q + j, d[i]) is then the dot product of lane
+// 4q + j's own block with activation 4s + i.  Six products take a block's 24
+// values for four activations; no sum crosses a block, so the block's scale
+// and class factor still multiply its f32 dot product.  No operand needs
+// zeros: a row past NB, or a stand-in lane past the unit's columns, reads
+// some staged activation, and only its own row or column of D sees it, which
+// is discarded.  The matrix core sums a block's products in its own order, so
+// outputs are within rounding of the single GEMV's; activation b always sits
+// in row b mod 4 of product set b / 4, so they are bit-identical across batch
+// widths.
 // XPER: activation blocks each thread stages through registers in the ordered
 // prologue (1 when the workgroup's threads cover every block, else 2; more
 // blocks go through the unordered loop first).
@@ -883,9 +891,8 @@ __host__ __device__ constexpr bool red_in_x(int nb_vectors, int xblocks, int wav
 // PHASE: a measurement launch that records kPhaseStamps real-time stamps per
 // workgroup (lane 0 of the stamping wave, a vector store each); the work is
 // the plain launch's.
-template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false, int PRO = 0,
-          bool PHASE = false, bool MX = false>
-__global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
+template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT, int PRO, bool PHASE, bool MX>
+__device__ __forceinline__ void gemv_body(const GemvArgs& a) {
   static_assert(!MX || (NB > 1 && LAYOUT == LEECH_PLANES14 && !ROT && !PHASE),
                 "matrix-core products serve batched Planes14 launches");
   constexpr int kPrefetch = pro_prefetch(PRO);        // units in flight per wave
@@ -901,7 +908,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   const int groups = (int)a.groups, C = a.C, waves = a.waves;   // unit counts fit 32 bits
   const int xblocks = groups * C;
   uint32_t* xs = (uint32_t*)xbase;                                 // NB × xblocks × 12 x pairs
-  uint8_t* p = xbase + (size_t)(NB * xblocks + (MX ? 1 : 0)) * 48;  // MX: and a zero block
+  uint8_t* p = xbase + (size_t)NB * xblocks * 48;
   uint32_t* cws = (uint32_t*)p;                                    // Golay70: 128 words
   u32x2a* p14t = (u32x2a*)(p + 128 * 4);                           // Golay70: 512 tables
   if constexpr (LAYOUT == LEECH_GOLAY70) p += kG70LdsBytes;
@@ -923,9 +930,8 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   };
   if (wave == 0) stamp(0);
-  // MX: lanes by column, each column's lanes padded to a multiple of 16
-  const int Rp = (a.R + 15) & ~15;
-  const int rl = MX ? lane % Rp : lane / C, cl = MX ? lane / Rp : lane % C;
+  // MX: lanes by column
+  const int rl = MX ? lane % a.R : lane / C, cl = MX ? lane / a.R : lane % C;
   const int gf = groups - 1;                      // full-width column groups
   const int C_last = (int)(nb - (int64_t)gf * C);
   const bool row_ok = rl < R_t && (!MX || cl < C), last_ok = row_ok && cl < C_last;
@@ -976,10 +982,9 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if constexpr (NB > 1) {
     // A batched launch stages all its activations here, kXChunk blocks a
     // thread in flight at a time: vector b's blocks follow vector b − 1's,
-    // zero past nb and for vectors past nbatch (MX: and the zero block after
-    // them).  (Requested after the first records instead, they return behind
+    // zero past nb and for vectors past nbatch.  (Requested after the first records instead, they return behind
     // them: loads return in order, and the launch is slower.)
-    const int total = NB * xblocks + (MX ? 1 : 0);
+    const int total = NB * xblocks;
     for (int j0 = tid; j0 < total; j0 += kXChunk * nthr) {
       XBlock r[kXChunk];
 #pragma unroll
@@ -1244,21 +1249,17 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   float acc[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) acc[b] = 0.0f;
-  // MX: the A operand's LDS byte address for product set s is
-  // x_on · (unit's x offset) + x_off[s]: activation 4s + m % 4 of the group's
-  // column for a lane on the diagonal (row group m / 4 = its group q, the
-  // activation below NB, a column of the unit), else the zero block
+  // MX: the A operand's LDS byte address for product set s is the unit's x
+  // offset + x_off[s]: lane 4q + i reads activation 4s + i (the last one past
+  // NB) of its column (the unit's first past the columns)
   constexpr int kSets = MX ? (NB + 3) / 4 : 1;
-  uint32_t x_on = 0u, x_off[kSets];
+  uint32_t x_off[kSets];
   if constexpr (MX) {
-    const int m = lane & 15, q = lane >> 4;
     const uint32_t x0 = (uint32_t)(xbase - smem);
-    const uint32_t zero = x0 + (uint32_t)(NB * xblocks * 48);
-    const bool on = (m >> 2) == q && (m & 3) < NB && cl < C;
-    x_on = on ? 1u : 0u;
+    const int i = min(lane & 3, NB - 1), c = min(cl, C - 1);
 #pragma unroll
     for (int s = 0; s < kSets; ++s)
-      x_off[s] = on ? x0 + (uint32_t)(((4 * s + (m & 3)) * xblocks + cl) * 48) : zero;
+      x_off[s] = x0 + (uint32_t)(((4 * s + i) * xblocks + c) * 48);
   }
   // One unit: decode slot p for unit g and accumulate.  LAST: the last
   // column group, whose stand-in lanes (past the last column) must add zero.
@@ -1269,16 +1270,17 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
       decode_block<LAYOUT>(pr, tile, tab, tab14, cw, side, h, e16, te);
       const float sf = (float)as_half(pr.scale) * te.factor;
       const uint32_t ub = (uint32_t)(g * (C * 48));
-      const u32x4a w0 = {h[0], h[1], h[2], h[3]}, w1 = {h[4], h[5], h[6], h[7]},
-                   w2 = {h[8], h[9], h[10], h[11]};
 #pragma unroll
       for (int s = 0; s < kSets; ++s) {
-        const u32x4a* xa =
-            (const u32x4a*)__builtin_assume_aligned(smem + (__umul24(x_on, ub) + x_off[s]), 16);
+        const u32x4a* xa = (const u32x4a*)__builtin_assume_aligned(smem + (ub + x_off[s]), 16);
+        const u32x4a a0 = xa[0], a1 = xa[1], a2 = xa[2];
         f32x4a d = {0.0f, 0.0f, 0.0f, 0.0f};
-        d = mfma16(xa[0], w0, d);
-        d = mfma16(xa[1], w1, d);
-        d = mfma16(xa[2], w2, d);
+        d = mfma4(a0.x, a0.y, h[0], h[1], d);
+        d = mfma4(a0.z, a0.w, h[2], h[3], d);
+        d = mfma4(a1.x, a1.y, h[4], h[5], d);
+        d = mfma4(a1.z, a1.w, h[6], h[7], d);
+        d = mfma4(a2.x, a2.y, h[8], h[9], d);
+        d = mfma4(a2.z, a2.w, h[10], h[11], d);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           if (4 * s + i < NB) acc[4 * s + i] = __builtin_fmaf(sf, d[i], acc[4 * s + i]);
@@ -1386,7 +1388,7 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
   if (red_x) __syncthreads();     // every wave is done with the activations
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const float v = MX ? row_sum_cols(acc[b], C, Rp) : row_sum(acc[b], C);
+    const float v = MX ? row_sum_cols(acc[b], C, a.R) : row_sum(acc[b], C);
     if (cl == 0 && rl < R_t) red[(b * waves + wave) * 64 + rl] = v;
   }
   __syncthreads();
@@ -1399,6 +1401,21 @@ __global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
     }
   }
   if (wave == 0) stamp(10);
+}
+
+template <int LAYOUT, bool EVEN, int NB = 1, int XPER = 2, bool ROT = false, int PRO = 0,
+          bool PHASE = false, bool MX = false>
+__global__ __launch_bounds__(kMaxWaves * 64) void gemv_kernel(GemvArgs a) {
+  gemv_body<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>(a);
+}
+
+// Matrix-core batches of 2 and 4 activations: held to 128 registers (four
+// waves per SIMD), so that two 8-wave workgroups share a CU when there are
+// more tiles than CUs.  Wider batches would spill there, and their staged
+// activations mostly leave LDS for one workgroup a CU anyway.
+template <int LAYOUT, bool EVEN, int NB, int XPER>
+__global__ __launch_bounds__(kMaxWaves * 64, 4) void gemv_kernel_mx(GemvArgs a) {
+  gemv_body<LAYOUT, EVEN, NB, XPER, false, 0, false, true>(a);
 }
 
 // --------------------------------------------------------- decode export
@@ -1550,11 +1567,11 @@ static bool even_bases(const GemvArgs& a, int layout) {
   return (rows_last * a.C * stride) % 4 == 0;
 }
 
-template <int LAYOUT, int NB = 1, bool MX = false>
+template <int LAYOUT, int NB = 1>
 static size_t gemv_lds_bytes(const GemvArgs& a) {
   const size_t red = red_in_x(NB, a.groups * a.C, a.waves) ? 0 : (size_t)NB * a.waves * 64 * 4;
   const size_t table = LAYOUT == kNoWeights ? 0 : (a.tab2 ? 2 : 1) * (size_t)a.tab_bytes;
-  return table + ((size_t)NB * a.groups * a.C + (MX ? 1 : 0)) * 48 +
+  return table + (size_t)NB * a.groups * a.C * 48 +
          (LAYOUT == LEECH_GOLAY70 ? kG70LdsBytes : 0) +
          (has_units<LAYOUT>() ? (size_t)a.groups * kUnitEntryBytes : 0) +
          red;
@@ -1563,13 +1580,22 @@ static size_t gemv_lds_bytes(const GemvArgs& a) {
 template <int LAYOUT, bool EVEN, int NB, int XPER, bool ROT = false, int PRO = 0,
           bool PHASE = false, bool MX = false>
 static int launch_gemv_kernel(const GemvArgs& a, size_t shmem, hipStream_t st) {
-  const void* fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>;
+  constexpr bool kCapped = MX && NB <= 4;
+  const void* fn;
+  if constexpr (kCapped)
+    fn = (const void*)gemv_kernel_mx<LAYOUT, EVEN, NB, XPER>;
+  else
+    fn = (const void*)gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>;
   if (shmem > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)shmem);
     if (e != hipSuccess) return hip_fail("hipFuncSetAttribute", e);
   }
-  hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>),
-                     dim3((unsigned)a.tiles), dim3(64 * a.waves), shmem, st, a);
+  if constexpr (kCapped)
+    hipLaunchKernelGGL((gemv_kernel_mx<LAYOUT, EVEN, NB, XPER>), dim3((unsigned)a.tiles),
+                       dim3(64 * a.waves), shmem, st, a);
+  else
+    hipLaunchKernelGGL((gemv_kernel<LAYOUT, EVEN, NB, XPER, ROT, PRO, PHASE, MX>),
+                       dim3((unsigned)a.tiles), dim3(64 * a.waves), shmem, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail("gemv launch", e);
   return LEECH_OK;
@@ -1626,7 +1652,7 @@ static int launch_gemv(const GemvArgs& a0, hipStream_t st) {
       }
     }
   }
-  const size_t shmem = gemv_lds_bytes<LAYOUT, NB, MX>(a);
+  const size_t shmem = gemv_lds_bytes<LAYOUT, NB>(a);
   if (shmem > 160 * 1024)
     return set_error(LEECH_E_SHAPE, "Kpad too large for the LDS-staged activation");
   if (LAYOUT == kNoWeights || even_bases(a, LAYOUT))
@@ -1662,16 +1688,13 @@ static int batch_width(const GemvArgs& a, int left, bool mx) {
                         : w == 8 ? gemv_lds_bytes<LEECH_PLANES14, 8>(a)
                         : w == 4 ? gemv_lds_bytes<LEECH_PLANES14, 4>(a)
                                  : gemv_lds_bytes<LEECH_PLANES14, 2>(a);
-    if (need + (mx ? 48 : 0) <= 160 * 1024) return w;     // mx: and the zero block
+    if (need <= 160 * 1024) return w;
   }
   return 1;
 }
 
-// Products of batched launches: the matrix cores where the geometry allows, or
-// v_dot2 per activation.  The matrix-core form places lanes by column, each
-// column's lanes padded to a multiple of 16 (one block column per
-// quarter-wave), so it needs lane_cols · 16·ceil(tile_rows / 16) ≤ 64.
-static bool batch_on_matrix_cores(int C, int R) { return C * ((R + 15) / 16 * 16) <= 64; }
+// Products of batched launches: the 16-block 4×4×4 MFMA form (default) or
+// v_dot2 per activation.
 static std::atomic<int> g_batch_mode{LEECH_BATCH_AUTO};
 
 template <int NB>
@@ -1770,8 +1793,7 @@ int leech_gemv_batch(const leech_layout_desc* desc, const void* d_main, const vo
   a.ldx = ldx;
   a.ldy = ldy;
   const hipStream_t st = (hipStream_t)stream;
-  const bool mx = batch > 1 && g_batch_mode.load(std::memory_order_relaxed) == LEECH_BATCH_AUTO &&
-                  batch_on_matrix_cores(a.C, a.R);
+  const bool mx = batch > 1 && g_batch_mode.load(std::memory_order_relaxed) == LEECH_BATCH_AUTO;
   for (int b0 = 0; b0 < batch;) {
     const int w = batch_width(a, batch - b0, mx);
     GemvArgs c = a;

@@ -1,7 +1,6 @@
 """Batched GEMV (Planes14) through the C ABI.  With v_dot2 products
-(BATCH_DOT2, and geometries the matrix-core form does not take) every
-output vector is bit-identical to the single GEMV of its activation; with the
-matrix-core products (BATCH_AUTO where lane_cols · 16·ceil(tile_rows/16) ≤ 64) each
+(BATCH_DOT2) every output vector is bit-identical to the single GEMV of its
+activation; with the matrix-core products (BATCH_AUTO, every geometry) each
 vector is within tolerance of the oracle's f64 product and of its single
 GEMV, and bit-identical whatever the batch size and its position in the
 batch.  Batches not a power of two, above 16, wide K (narrower chunks), every
@@ -66,7 +65,7 @@ def build(dev, dcb, M, K, seed, geometry=None):
 
 
 def matrix_cores(mat, B):
-    return B > 1 and mat.batch_on_matrix_cores
+    return B > 1
 
 
 @pytest.fixture
@@ -130,27 +129,22 @@ def test_batch_matches_oracle_and_single(dev, dcb, M, K, B):
     check_auto(dev, mat, inp, X, Y)
 
 
-# every placement the matrix-core path takes: one column per group of lanes
-# (C = 1, R = 16..64), two and four columns, three columns with a lane group
-# past the last column (C = 3, R = 16), and R · C < 64; columns padded to 16
-# lanes (R = 28, 24, 20, 12, 60, 4: lanes r ≥ R hold stand-ins); ragged last
-# tiles and last column groups; and geometries the form cannot take (3 × 20,
-# 8 × 8, 16 × 4: v_dot2, bit-identical to single GEMVs)
+# lane placements of the matrix-core path: every lane_cols (1, 2, 3, 4, 8, 16),
+# tile_rows from 4 to 64, lanes past the last column (R · C < 64), ragged last
+# tiles (rows of a 4-lane block partly past the matrix) and last column groups
 MX_GEOMETRIES = [((1, 64), 1000, 24 * 37), ((2, 32), 777, 24 * 41), ((4, 16), 301, 24 * 43),
                  ((3, 16), 333, 24 * 29), ((1, 16), 70, 24 * 11), ((1, 48), 100, 24 * 7),
                  ((2, 16), 50, 24 * 9), ((1, 32), 33, 24), ((4, 16), 4096, 4104),
                  ((2, 28), 1000, 24 * 45), ((2, 24), 301, 24 * 50), ((1, 20), 333, 24 * 13),
                  ((4, 12), 100, 24 * 23), ((1, 60), 777, 24 * 17), ((3, 12), 200, 24 * 31),
                  ((4, 4), 37, 24 * 9), ((3, 20), 301, 24 * 50), ((8, 8), 100, 24 * 37),
-                 ((16, 4), 30, 24 * 70)]
+                 ((16, 4), 30, 24 * 70), ((8, 4), 66, 24 * 20), ((3, 20), 5120, 5136)]
 
 
 @pytest.mark.parametrize("geo,M,K", MX_GEOMETRIES)
 def test_matrix_core_geometries(dev, dcb, geo, M, K):
     inp, mat = build(dev, dcb, M, K, M + K, geometry=geo)
     assert (mat.desc.lane_cols, mat.desc.tile_rows) == geo
-    C, R = geo
-    assert mat.batch_on_matrix_cores == (C * (-(-R // 16) * 16) <= 64)
     for B in (2, 3, 5, 16, 17):
         say(f"[batch mx] {geo} {M}x{K} B={B}")
         X = activations(K, B, seed=K + B)
@@ -159,7 +153,8 @@ def test_matrix_core_geometries(dev, dcb, geo, M, K):
 
 
 @pytest.mark.parametrize("geo,M,K", [((4, 16), 301, 24 * 43), ((2, 32), 777, 24 * 41),
-                                     ((1, 64), 1000, 24 * 37), ((2, 28), 1000, 24 * 45)])
+                                     ((1, 64), 1000, 24 * 37), ((2, 28), 1000, 24 * 45),
+                                     ((3, 20), 301, 24 * 50), ((8, 8), 100, 24 * 37)])
 def test_matrix_core_bits_independent_of_batch(dev, dcb, geo, M, K):
     """One activation's y is the same bits alone in a 2-wide launch, in
     every position of 4-, 8- and 16-wide launches and in a trailing chunk."""

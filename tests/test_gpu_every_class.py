@@ -180,18 +180,13 @@ def test_every_class_batched_grouped_rotated(dev, dcb, M, nb, sort_by_class):
         Yd = mat.gemv_batch(Xd, centroids=CEN).cpu().numpy()
     finally:
         P.set_batch_mode(P.BATCH_AUTO)
-    # matrix-core products where the geometry takes them: within
-    # 2^-15 · Σ|w x| of the single GEMV (the dot units' measured rounding);
-    # v_dot2 products: the single GEMV's bits
-    mx = mat.batch_on_matrix_cores
+    # matrix-core products: within 2^-15 · Σ|w x| of the single GEMV (the dot
+    # units' measured rounding); v_dot2 products: the single GEMV's bits
     for b in range(3):
         yb = mat.gemv(Xd[b].contiguous(), centroids=CEN).cpu().numpy()
         assert np.array_equal(Yd[b].view(np.uint32), yb.view(np.uint32)), b
-        if mx:
-            bound = 2.0 ** -15 * (np.abs(W) @ np.abs(X[b].astype(np.float64)))
-            assert (np.abs(Y[b].astype(np.float64) - yb) <= bound).all(), b
-        else:
-            assert np.array_equal(Y[b].view(np.uint32), yb.view(np.uint32)), b
+        bound = 2.0 ** -15 * (np.abs(W) @ np.abs(X[b].astype(np.float64)))
+        assert (np.abs(Y[b].astype(np.float64) - yb) <= bound).all(), b
         e = D.errors(Y[b], D.gemv64(W, X[b]), W, X[b])
         assert e["max_norm_err"] <= TOL_NORM and e["max_abs_err"] <= TOL_PAPER, (b, e)
     if M > 64:

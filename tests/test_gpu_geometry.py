@@ -7,11 +7,9 @@ that share a tile, through the C ABI.
   each layout decodes bit-exactly to the drawn points, all four layouts (and
   both exception decoders) give bit-identical y, and y is within the GEMV
   tolerance of the oracle's f64 matvec on every row.
-* The batched and rotated entry points on a three-column geometry (v_dot2
-  batches), and on two geometries whose batches run on the matrix cores with
-  padded lane columns (2 × 24, 1 × 60), give the single GEMV's bits (matrix
-  cores: within the dot units' rounding, and its bits in the v_dot2 mode) and
-  the two-call bits.
+* The batched and rotated entry points on 3 × 20, 2 × 24 and 1 × 60 give
+  the single GEMV's bits (batches: in the v_dot2 mode; on the matrix cores,
+  within the dot units' rounding) and the two-call bits.
 * Row groups whose boundaries fall inside tiles (each such tile holds rows of
   two groups, every lane reading its own row's centroids): every row matches
   the oracle with its own group's centroids, in every layout, bit-identical
@@ -115,12 +113,9 @@ def test_geometry_batched_and_rotated(dev, dcb, geo):
     for b in range(5):
         y1 = mat.gemv(Xt[b].contiguous(), centroids=CEN).cpu().numpy()
         assert np.array_equal(Yd[b].view(np.uint32), y1.view(np.uint32)), b
-        if mat.batch_on_matrix_cores:
-            # matrix-core products: within the dot units' rounding (2^-15 · Σ|w x|)
-            bound = 2.0 ** -15 * (np.abs(W) @ np.abs(X[b].astype(np.float64)))
-            assert (np.abs(Y[b].astype(np.float64) - y1) <= bound).all(), b
-        else:
-            assert np.array_equal(Y[b].view(np.uint32), y1.view(np.uint32)), b
+        # matrix-core products: within the dot units' rounding (2^-15 · Σ|w x|)
+        bound = 2.0 ** -15 * (np.abs(W) @ np.abs(X[b].astype(np.float64)))
+        assert (np.abs(Y[b].astype(np.float64) - y1) <= bound).all(), b
     raw = Xt[0, :K].contiguous()
     s = torch.from_numpy(synth.make_signs(K, seed=3, name="geometry-batch")).to(dev)
     y_rot = mat.gemv_rotated(raw, s, group_centroids=(CEN,)).cpu().numpy()

@@ -79,16 +79,15 @@ def test_random_shape(dev, dcb, i):
                             for b in range(2)])
     Xd = torch.from_numpy(X).to(dev)
     Y = p14.gemv_batch(Xd, centroids=CEN).cpu().numpy()
-    if p14.batch_on_matrix_cores:
-        # matrix-core products: within 2^-15 · Σ|w x| of the single GEMV (the
-        # dot units' measured rounding), and the v_dot2 mode gives its bits
-        bound = 2.0 ** -15 * (np.abs(W) @ np.abs(inp.x.astype(np.float64)))
-        assert (np.abs(Y[0][rows].astype(np.float64) - y1[rows]) <= bound).all()
-        P.set_batch_mode(P.BATCH_DOT2)
-        try:
-            Y = p14.gemv_batch(Xd, centroids=CEN).cpu().numpy()
-        finally:
-            P.set_batch_mode(P.BATCH_AUTO)
+    # matrix-core products: within 2^-15 · Σ|w x| of the single GEMV (the dot
+    # units' measured rounding), and the v_dot2 mode gives its bits
+    bound = 2.0 ** -15 * (np.abs(W) @ np.abs(inp.x.astype(np.float64)))
+    assert (np.abs(Y[0][rows].astype(np.float64) - y1[rows]) <= bound).all()
+    P.set_batch_mode(P.BATCH_DOT2)
+    try:
+        Y = p14.gemv_batch(Xd, centroids=CEN).cpu().numpy()
+    finally:
+        P.set_batch_mode(P.BATCH_AUTO)
     assert np.array_equal(Y[0].view(np.uint32), y1.view(np.uint32))
     # grouped, one group: the plain call's bits
     yg = p14.gemv_grouped(x, [M], [CEN]).cpu().numpy()
