@@ -309,11 +309,12 @@ int leech_gemv(const leech_layout_desc* desc, const void* d_main, const void* d_
  * launch and multiplied with up to 16 activations staged in LDS; larger
  * batches run in chunks of 16 (fewer where Kpad leaves too little LDS: 16
  * activations fit up to about Kpad = 4,600, 8 up to about 9,200, the exact
- * bound depending on the column groups' rounding).  Products as
- * leech_set_batch_mode selects: on the matrix cores (the default) Y[b] is
- * within rounding of leech_gemv on X[b]
- * and a single vector left after the 16-wide chunks still runs 2 wide; with
- * v_dot2 Y[b] is bit-identical to leech_gemv on X[b].  batch > 1 serves
+ * bound depending on the column groups' rounding; where not even two fit,
+ * the vectors run as single GEMVs).  Products as leech_set_batch_mode
+ * selects: on the matrix cores (the default) Y[b][r] is within rounding of
+ * leech_gemv on X[b] (tested within 2^-15 · Σ_j |W_rj · X[b]_j|), and a single
+ * vector left after the 16-wide chunks still runs 2 wide; with v_dot2 Y[b]
+ * is bit-identical to leech_gemv on X[b].  batch > 1 serves
  * LEECH_PLANES14 (LEECH_E_LAYOUT otherwise) and needs ldx ≥ Kpad, ldx a
  * multiple of 8 and ldy ≥ M (LEECH_E_ARG); batch = 1 is leech_gemv.  Other
  * arguments as leech_gemv. */
